@@ -1,0 +1,270 @@
+"""CPU oracle for BF16 component-product emulation of FP32/FP64 GEMM (arxiv 2609.04663).
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package.  It shares no code
+with the HIP implementation in ``paper_2609_04663_amd``: the arithmetic lives in
+``oracle.c`` (plain C, FP64 where the paper does not fix the precision), and this
+module only marshals numpy arrays through ctypes and evaluates the paper's
+accuracy metrics.
+
+Functions (all operands row-major numpy arrays, all on the host):
+
+* ``split_f32(X)``       -> uint16 [3, R, C]     Eq. (fp32split), Sec. 4.2
+* ``split_f64(X, mode)`` -> (uint16 [6, R, C], v[6], residual A^(6), status)
+                                                  Eq. (fp64split), Sec. 4.3
+* ``emu_sgemm(A, B)``    -> FP32 C               Algorithm fp32 + Sec. 6.2/6.3 order
+* ``emu_dgemm(A, B, nprod, mode)`` -> FP64 C     Algorithm fp64, Eq. (fp64reconstruction)
+* ``*_entries``          -> the same for selected (row, col) entries
+* ``ref_gemm_f64``, ``ref_gemm_dd``, ``ref_dd_entries`` -> references
+* ``e_F``, ``e_scaled``  -> Eq. (froerror) and Eq. (scalederror), Sec. 7.3
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+SPLIT_SYM = 0
+SPLIT_LITERAL = 1
+KC = 256  # reduction-panel length B_K of the paper's blocked loop (Sec. 6.1)
+
+ST_NAN, ST_RANGE, ST_SUBNORMAL, ST_OVERFLOW, ST_INEXACT32 = 1, 2, 4, 8, 16
+NPROD_TO_D = {6: 3, 10: 4, 15: 5, 21: 6}
+
+
+def build(force: bool = True) -> str:
+    """Compile oracle.c with gcc (no fast-math, no FMA contraction)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-fopenmp", "-ffp-contract=off", "-fno-fast-math", "-std=c11",
+               "-Wall", "-shared", "-fPIC", _SRC, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        build(force=False)
+        L = ctypes.CDLL(_LIB)
+        i64, p, u32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_uint32
+        L.orc_bf16_rne_f32.argtypes = [ctypes.c_float]
+        L.orc_bf16_rne_f32.restype = ctypes.c_uint16
+        L.orc_bf16_rne_f64.argtypes = [ctypes.c_double]
+        L.orc_bf16_rne_f64.restype = ctypes.c_uint16
+        L.orc_split_f32.argtypes = [i64, i64, p, i64, p]
+        L.orc_split_f32.restype = u32
+        L.orc_split_f64.argtypes = [i64, i64, p, i64, ctypes.c_int, p, p, p]
+        L.orc_split_f64.restype = u32
+        L.orc_emu_sgemm.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, i64]
+        L.orc_emu_sgemm.restype = u32
+        L.orc_emu_sgemm_entries.argtypes = [i64, i64, i64, p, i64, p, i64, i64, p, p, p, i64]
+        L.orc_emu_sgemm_entries.restype = u32
+        L.orc_emu_dgemm.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, ctypes.c_int,
+                                    ctypes.c_int, i64]
+        L.orc_emu_dgemm.restype = u32
+        L.orc_emu_dgemm_entries.argtypes = [i64, i64, i64, p, i64, p, i64, i64, p, p, p,
+                                            ctypes.c_int, ctypes.c_int, i64]
+        L.orc_emu_dgemm_entries.restype = u32
+        L.orc_ref_gemm_f64.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64]
+        L.orc_ref_gemm_dd.argtypes = [i64, i64, i64, p, i64, p, i64, p, p, i64]
+        L.orc_ref_dd_entries.argtypes = [i64, i64, i64, p, i64, p, i64, i64, p, p, p, p]
+        L.orc_absprod_entries.argtypes = [i64, p, i64, p, i64, i64, p, p, p]
+        L.orc_num_threads.restype = ctypes.c_int
+        L.orc_dot_bf16_f32.argtypes = [i64, p, p]
+        L.orc_dot_bf16_f32.restype = ctypes.c_float
+        _lib = L
+    return _lib
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    a = np.asarray(a)
+    assert a.dtype == dtype, f"expected {dtype}, got {a.dtype}"
+    return np.ascontiguousarray(a)
+
+
+def num_threads() -> int:
+    return lib().orc_num_threads()
+
+
+def bf16_rne_f32(x: float) -> int:
+    return int(lib().orc_bf16_rne_f32(float(x)))
+
+
+def bf16_rne_f64(x: float) -> int:
+    return int(lib().orc_bf16_rne_f64(float(x)))
+
+
+def dot_bf16_f32(x_bits: np.ndarray, y_bits: np.ndarray) -> float:
+    """fl_32 of the exact dot product of two BF16 vectors (bit patterns)."""
+    x = np.ascontiguousarray(np.asarray(x_bits, dtype=np.uint16))
+    y = np.ascontiguousarray(np.asarray(y_bits, dtype=np.uint16))
+    assert x.shape == y.shape
+    return float(lib().orc_dot_bf16_f32(x.size, _ptr(x), _ptr(y)))
+
+
+def bf16_to_f32(h: np.ndarray) -> np.ndarray:
+    """Exact value of BF16 bit patterns (upper half of binary32)."""
+    return (np.asarray(h, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def split_f32(X: np.ndarray):
+    X = _c(X, np.float32)
+    R, C = X.shape
+    out = np.zeros((3, R, C), dtype=np.uint16)
+    st = lib().orc_split_f32(R, C, _ptr(X), C, _ptr(out))
+    return out, int(st)
+
+
+def split_f64(X: np.ndarray, mode: int = SPLIT_SYM):
+    X = _c(X, np.float64)
+    R, C = X.shape
+    out = np.zeros((6, R, C), dtype=np.uint16)
+    v = np.zeros(6, dtype=np.int32)
+    res = np.zeros((R, C), dtype=np.float64)
+    st = lib().orc_split_f64(R, C, _ptr(X), C, int(mode), _ptr(out), _ptr(v), _ptr(res))
+    return out, v, res, int(st)
+
+
+def emu_sgemm(A: np.ndarray, B: np.ndarray, kc: int = KC):
+    A, B = _c(A, np.float32), _c(B, np.float32)
+    M, K = A.shape
+    K2, N = B.shape
+    assert K == K2
+    C = np.zeros((M, N), dtype=np.float32)
+    st = lib().orc_emu_sgemm(M, N, K, _ptr(A), K, _ptr(B), N, _ptr(C), N, int(kc))
+    return C, int(st)
+
+
+def _idx(rows, cols):
+    r = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
+    c = np.ascontiguousarray(np.asarray(cols, dtype=np.int64))
+    assert r.shape == c.shape
+    return r, c
+
+
+def emu_sgemm_entries(A, B, rows, cols, kc: int = KC):
+    A, B = _c(A, np.float32), _c(B, np.float32)
+    M, K = A.shape
+    N = B.shape[1]
+    r, c = _idx(rows, cols)
+    out = np.zeros(r.shape, dtype=np.float32)
+    st = lib().orc_emu_sgemm_entries(M, N, K, _ptr(A), K, _ptr(B), N, r.size, _ptr(r), _ptr(c),
+                                     _ptr(out), int(kc))
+    return out, int(st)
+
+
+def emu_dgemm(A: np.ndarray, B: np.ndarray, nprod: int, mode: int = SPLIT_SYM, kc: int = KC):
+    A, B = _c(A, np.float64), _c(B, np.float64)
+    M, K = A.shape
+    K2, N = B.shape
+    assert K == K2 and nprod in NPROD_TO_D
+    C = np.zeros((M, N), dtype=np.float64)
+    st = lib().orc_emu_dgemm(M, N, K, _ptr(A), K, _ptr(B), N, _ptr(C), N, int(nprod), int(mode),
+                             int(kc))
+    return C, int(st)
+
+
+def emu_dgemm_entries(A, B, rows, cols, nprod: int, mode: int = SPLIT_SYM, kc: int = KC):
+    A, B = _c(A, np.float64), _c(B, np.float64)
+    M, K = A.shape
+    N = B.shape[1]
+    r, c = _idx(rows, cols)
+    out = np.zeros(r.shape, dtype=np.float64)
+    st = lib().orc_emu_dgemm_entries(M, N, K, _ptr(A), K, _ptr(B), N, r.size, _ptr(r), _ptr(c),
+                                     _ptr(out), int(nprod), int(mode), int(kc))
+    return out, int(st)
+
+
+def ref_gemm_f64(A, B):
+    A = np.ascontiguousarray(np.asarray(A, dtype=np.float64))
+    B = np.ascontiguousarray(np.asarray(B, dtype=np.float64))
+    M, K = A.shape
+    N = B.shape[1]
+    C = np.zeros((M, N), dtype=np.float64)
+    lib().orc_ref_gemm_f64(M, N, K, _ptr(A), K, _ptr(B), N, _ptr(C), N)
+    return C
+
+
+def ref_gemm_dd(A, B):
+    """Double-double reference: returns (hi, lo) with C ~ hi + lo."""
+    A = np.ascontiguousarray(np.asarray(A, dtype=np.float64))
+    B = np.ascontiguousarray(np.asarray(B, dtype=np.float64))
+    M, K = A.shape
+    N = B.shape[1]
+    hi = np.zeros((M, N), dtype=np.float64)
+    lo = np.zeros((M, N), dtype=np.float64)
+    lib().orc_ref_gemm_dd(M, N, K, _ptr(A), K, _ptr(B), N, _ptr(hi), _ptr(lo), N)
+    return hi, lo
+
+
+def ref_dd_entries(A, B, rows, cols):
+    A = np.ascontiguousarray(np.asarray(A, dtype=np.float64))
+    B = np.ascontiguousarray(np.asarray(B, dtype=np.float64))
+    M, K = A.shape
+    N = B.shape[1]
+    r, c = _idx(rows, cols)
+    hi = np.zeros(r.shape, dtype=np.float64)
+    lo = np.zeros(r.shape, dtype=np.float64)
+    lib().orc_ref_dd_entries(M, N, K, _ptr(A), K, _ptr(B), N, r.size, _ptr(r), _ptr(c),
+                             _ptr(hi), _ptr(lo))
+    return hi, lo
+
+
+def absprod_entries(A, B, rows, cols):
+    """(|A||B|)_ij in FP64 for the selected entries (scaled-error denominator)."""
+    A = np.ascontiguousarray(np.asarray(A, dtype=np.float64))
+    B = np.ascontiguousarray(np.asarray(B, dtype=np.float64))
+    K = A.shape[1]
+    N = B.shape[1]
+    r, c = _idx(rows, cols)
+    out = np.zeros(r.shape, dtype=np.float64)
+    lib().orc_absprod_entries(K, _ptr(A), K, _ptr(B), N, r.size, _ptr(r), _ptr(c), _ptr(out))
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Accuracy metrics, Sec. 7.3.
+
+def _diff(Chat, ref):
+    """Chat - ref, with ref either an array or a (hi, lo) double-double pair."""
+    Chat = np.asarray(Chat, dtype=np.float64)
+    if isinstance(ref, tuple):
+        hi, lo = ref
+        return (Chat - hi) - lo, hi + lo
+    ref = np.asarray(ref, dtype=np.float64)
+    return Chat - ref, ref
+
+
+def e_F(Chat, ref) -> float:
+    """Frobenius-norm relative error, Eq. (froerror)."""
+    d, r = _diff(Chat, ref)
+    den = float(np.linalg.norm(r.ravel()))
+    return float(np.linalg.norm(d.ravel())) / den if den > 0 else float("nan")
+
+
+def e_scaled(Chat, ref, absprod):
+    """GEMM-scaled componentwise error, Eq. (scalederror).
+
+    Returns (max over entries with a nonzero denominator, max absolute error over
+    entries whose denominator is zero) -- the latter reported separately."""
+    d, _ = _diff(Chat, ref)
+    den = np.asarray(absprod, dtype=np.float64)
+    nz = den > 0
+    scaled = float(np.max(np.abs(d[nz]) / den[nz])) if nz.any() else 0.0
+    zero_abs = float(np.max(np.abs(d[~nz]))) if (~nz).any() else 0.0
+    return scaled, zero_abs
