@@ -1,0 +1,134 @@
+/*
+ * emu.h -- C ABI of the MI355X (gfx950) library for FP32 and FP64 GEMM
+ * emulated through BF16 component products (arxiv 2609.04663).
+ *
+ * Problem (Sec. 3.2, Eq. gemm): C = A B with A (M x K), B (K x N), C (M x N),
+ * all row-major with leading dimensions lda, ldb, ldc counted in elements.
+ * There is no alpha/beta and no transpose: C is fully overwritten.
+ *
+ * Pointers.  A, B and C are device pointers (HIP global memory) owned by the
+ * caller; A and B are only read.  C must not alias A or B.  Every call is
+ * ordered on the library's current stream (emu_set_stream) and returns
+ * without synchronising the host; results are ready when that stream is.
+ *
+ * Workspace.  The library keeps one device workspace per process (packed BF16
+ * component planes, per-level exponents, a status word).  It is grown with
+ * hipMalloc when a call needs more than it holds -- never on a call whose
+ * sizes fit -- and freed by emu_release_workspace.  The environment variable
+ * EMU_WORKSPACE_LIMIT (bytes) caps its size; a call that would exceed the cap
+ * returns EMU_ENOMEM.
+ *
+ * Return codes.  EMU_OK on success.  EMU_EINVAL for a bad argument (checked
+ * before any HIP call, nothing is launched): M, N or K negative; lda < K,
+ * ldb < N, ldc < N (each at least 1); a NULL pointer for an operand with a
+ * nonzero extent; nprod not in {6, 10, 15, 21}.  EMU_EHIP when a HIP runtime
+ * call or kernel launch fails (message in emu_last_error).  EMU_ENOMEM when the
+ * workspace cannot be allocated.
+ *
+ * Degenerate sizes.  M == 0 or N == 0: nothing is done.  K == 0: C = 0.
+ *
+ * Input domain.  FP32 inputs: any finite value; the three-component split is
+ * exact for 2^-103 <= |a| < (2 - 2^-8) 2^127 (Sec. 4.2).  FP64 inputs: the
+ * BF16-range domain of Eq. (bf16rangefp64) -- 0 or 2^-126 <= |x| <=
+ * (2 - 2^-7) 2^127 -- with every extracted slice a normal BF16 value
+ * (Sec. 3.1, 4.3).  As in the paper there is no fallback: out-of-domain input
+ * is computed anyway and reported through emu_domain_status; the call itself
+ * does not fail.
+ *
+ * Not thread-safe: one host thread at a time may call into the library.
+ */
+#ifndef EMU_H
+#define EMU_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define EMU_OK 0
+#define EMU_EINVAL 1
+#define EMU_EHIP 2
+#define EMU_ENOMEM 3
+
+/* Status bits reported by emu_domain_status. */
+#define EMU_STATUS_NAN 1u       /* NaN or infinity in an operand */
+#define EMU_STATUS_RANGE 2u     /* finite FP64 input outside Eq. (bf16rangefp64) */
+#define EMU_STATUS_SUBNORMAL 4u /* a nonzero component is subnormal in BF16 or
+                                   underflowed (the split is not exact) */
+#define EMU_STATUS_OVERFLOW 8u  /* a component overflowed BF16 */
+
+/* FP64 split projection constant (Eq. fp64split).  SYM (default) uses
+   Sigma = 0.75 * 2^(v+45): granularity 2^(v-8) for both signs, which is the
+   reading that reproduces the paper's accuracy table.  LITERAL uses
+   Sigma = 2^(v+45) exactly as printed. */
+#define EMU_SPLIT_SYM 0
+#define EMU_SPLIT_LITERAL 1
+
+/* Emulated SGEMM, Algorithm fp32 (Sec. 4.2, Eq. fp32split and fp32six):
+   each FP32 operand is split into three BF16 components; the six products
+   A_iB_j with i + j < 3 are evaluated with FP32 accumulation on bf16 MFMA and
+   combined in FP32 per reduction panel of 256.  A: M x K (lda), B: K x N
+   (ldb), C: M x N (ldc), device pointers, FP32. */
+int emu_sgemm(int64_t M, int64_t N, int64_t K, const float *A, int64_t lda, const float *B,
+              int64_t ldb, float *C, int64_t ldc);
+
+/* Emulated DGEMM, Algorithm fp64 (Sec. 4.3, Eq. fp64split, fp64productcounts,
+   fp64reconstruction): each FP64 operand gets the fixed six-slice Ozaki split
+   with operand-wide exponents; the nprod products with i + j < d
+   (nprod = 6, 10, 15, 21 for d = 3, 4, 5, 6) are each formed in FP32 per
+   reduction panel of 256 (exactly, see below), widened and added in FP64 in
+   the order: panel ascending, diagonal i + j ascending, i ascending.
+   A: M x K (lda), B: K x N (ldb), C: M x N (ldc), device pointers, FP64.
+   For in-domain inputs every panel product is an exact FP32 value, so the
+   result is independent of the order of the bf16 MFMA accumulation inside a
+   panel. */
+int emu_dgemm(int64_t M, int64_t N, int64_t K, const double *A, int64_t lda, const double *B,
+              int64_t ldb, double *C, int64_t ldc, int nprod);
+
+/* Stream for subsequent calls (a hipStream_t); NULL selects the default
+   stream.  Always returns EMU_OK. */
+int emu_set_stream(void *hip_stream);
+
+/* Projection constant of the FP64 split for subsequent emu_dgemm and
+   emu_split_f64 calls: EMU_SPLIT_SYM (default) or EMU_SPLIT_LITERAL.
+   EMU_EINVAL for any other value. */
+int emu_set_split_mode(int mode);
+
+/* Synchronises the current stream, stores in *flags the EMU_STATUS_* bits
+   accumulated by all calls since the previous emu_domain_status, and clears
+   them.  EMU_EINVAL if flags is NULL. */
+int emu_domain_status(unsigned *flags);
+
+/* Message of the last failing call (empty string if none).  Owned by the
+   library, valid until the next call. */
+const char *emu_last_error(void);
+
+/* Frees the workspace (synchronises the device first).  The next call
+   allocates again. */
+int emu_release_workspace(void);
+
+/* Bytes currently held by the workspace (0 after emu_release_workspace). */
+int64_t emu_workspace_bytes(void);
+
+/* Test hook: the FP32 split of Eq. (fp32split) as the GEMM consumes it.
+   X is an R x Cc row-major FP32 device matrix (ldx).  as_b = 0 runs the
+   A-operand pack (rows of X are GEMM rows), as_b = 1 the B-operand pack (X is
+   K x N and is packed transposed).  comps (device, uint16 BF16 bit patterns)
+   receives [3][R][Cc], plane-major, in X's own orientation, unpacked from the
+   packed buffer.  Errors as above. */
+int emu_split_f32(int64_t R, int64_t Cc, const float *X, int64_t ldx, int as_b, uint16_t *comps);
+
+/* Test hook: the FP64 split of Eq. (fp64split) as the GEMM consumes it.
+   X is R x Cc row-major FP64 (device, ldx); as_b as for emu_split_f32.
+   slices (device) receives [6][R][Cc] BF16 bit patterns; v (device, int32[6])
+   receives v^(r) = ceil(log2 max|X^(r)|) per level, INT32_MIN for a level
+   whose residual is identically zero. */
+int emu_split_f64(int64_t R, int64_t Cc, const double *X, int64_t ldx, int as_b,
+                  uint16_t *slices, int32_t *v);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EMU_H */

@@ -1,0 +1,162 @@
+"""Python binding of libemu: FP32/FP64 GEMM emulated through BF16 component
+products on AMD Instinct MI355X (gfx950), after arxiv 2609.04663.
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of ``libemu.so`` (C ABI in ``include/emu.h``).  PyTorch supplies the
+device memory and the stream; tensors must be CUDA (HIP) tensors, row-major
+with unit stride in the last dimension.  There is no CPU fallback: if the
+library is not built, importing the functions raises.
+
+    sgemm(A, B, C=None)            -> C = A @ B, FP32, 3 components / 6 products
+    dgemm(A, B, nprod, C=None)     -> C = A @ B, FP64, six slices / nprod products
+    split_f32(X, as_b=False)       -> int16 tensor [3, R, C] of BF16 bit patterns
+    split_f64(X, as_b=False)       -> (int16 tensor [6, R, C], int32 tensor [6])
+    domain_status()                -> EMU_STATUS_* bits accumulated since last call
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libemu.so")
+
+EMU_OK, EMU_EINVAL, EMU_EHIP, EMU_ENOMEM = 0, 1, 2, 3
+STATUS_NAN, STATUS_RANGE, STATUS_SUBNORMAL, STATUS_OVERFLOW = 1, 2, 4, 8
+SPLIT_SYM, SPLIT_LITERAL = 0, 1
+NPROD = (6, 10, 15, 21)
+
+EXPORTS = ("emu_sgemm", "emu_dgemm", "emu_set_stream", "emu_set_split_mode",
+           "emu_domain_status", "emu_last_error", "emu_release_workspace",
+           "emu_workspace_bytes", "emu_split_f32", "emu_split_f64")
+
+
+class EmuError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"libemu error {code}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libemu.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python -m paper_2609_04663_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        i64, p, ci = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+        L.emu_sgemm.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64]
+        L.emu_dgemm.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, ci]
+        L.emu_set_stream.argtypes = [p]
+        L.emu_set_split_mode.argtypes = [ci]
+        L.emu_domain_status.argtypes = [ctypes.POINTER(ctypes.c_uint)]
+        L.emu_last_error.restype = ctypes.c_char_p
+        L.emu_workspace_bytes.restype = i64
+        L.emu_split_f32.argtypes = [i64, i64, p, i64, ci, p]
+        L.emu_split_f64.argtypes = [i64, i64, p, i64, ci, p, p]
+        for name in ("emu_sgemm", "emu_dgemm", "emu_set_stream", "emu_set_split_mode",
+                     "emu_domain_status", "emu_release_workspace", "emu_split_f32",
+                     "emu_split_f64"):
+            getattr(L, name).restype = ci
+        _lib = L
+    return _lib
+
+
+def _check(rc: int):
+    if rc != EMU_OK:
+        raise EmuError(rc, lib().emu_last_error().decode())
+
+
+def _bind_stream(dev: torch.device):
+    lib().emu_set_stream(ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream))
+
+
+def _mat(t: torch.Tensor, dtype, name: str):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1) or t.stride(0) < max(1, t.shape[1]):
+        raise ValueError(f"{name} must be a row-major 2-D tensor with unit column stride")
+    return t
+
+
+def _ld(t: torch.Tensor) -> int:
+    return max(1, t.stride(0), t.shape[1])
+
+
+def sgemm(A: torch.Tensor, B: torch.Tensor, C: torch.Tensor | None = None) -> torch.Tensor:
+    _mat(A, torch.float32, "A")
+    _mat(B, torch.float32, "B")
+    M, K = A.shape
+    K2, N = B.shape
+    if K != K2:
+        raise ValueError("inner dimensions differ")
+    if C is None:
+        C = torch.empty((M, N), dtype=torch.float32, device=A.device)
+    _mat(C, torch.float32, "C")
+    _bind_stream(A.device)
+    _check(lib().emu_sgemm(M, N, K, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), C.data_ptr(),
+                           _ld(C)))
+    return C
+
+
+def dgemm(A: torch.Tensor, B: torch.Tensor, nprod: int,
+          C: torch.Tensor | None = None) -> torch.Tensor:
+    _mat(A, torch.float64, "A")
+    _mat(B, torch.float64, "B")
+    M, K = A.shape
+    K2, N = B.shape
+    if K != K2:
+        raise ValueError("inner dimensions differ")
+    if C is None:
+        C = torch.empty((M, N), dtype=torch.float64, device=A.device)
+    _mat(C, torch.float64, "C")
+    _bind_stream(A.device)
+    _check(lib().emu_dgemm(M, N, K, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), C.data_ptr(),
+                           _ld(C), int(nprod)))
+    return C
+
+
+def split_f32(X: torch.Tensor, as_b: bool = False) -> torch.Tensor:
+    _mat(X, torch.float32, "X")
+    R, Cc = X.shape
+    out = torch.empty((3, R, Cc), dtype=torch.int16, device=X.device)
+    _bind_stream(X.device)
+    _check(lib().emu_split_f32(R, Cc, X.data_ptr(), _ld(X), int(as_b), out.data_ptr()))
+    return out
+
+
+def split_f64(X: torch.Tensor, as_b: bool = False):
+    _mat(X, torch.float64, "X")
+    R, Cc = X.shape
+    out = torch.empty((6, R, Cc), dtype=torch.int16, device=X.device)
+    v = torch.empty(6, dtype=torch.int32, device=X.device)
+    _bind_stream(X.device)
+    _check(lib().emu_split_f64(R, Cc, X.data_ptr(), _ld(X), int(as_b), out.data_ptr(),
+                               v.data_ptr()))
+    return out, v
+
+
+def set_split_mode(mode: int):
+    _check(lib().emu_set_split_mode(int(mode)))
+
+
+def domain_status() -> int:
+    f = ctypes.c_uint(0)
+    _check(lib().emu_domain_status(ctypes.byref(f)))
+    return int(f.value)
+
+
+def release_workspace():
+    _check(lib().emu_release_workspace())
+
+
+def workspace_bytes() -> int:
+    return int(lib().emu_workspace_bytes())

@@ -1,0 +1,279 @@
+// Host side of the C ABI declared in include/emu.h: argument validation,
+// the device workspace, launch sequencing on the current stream, status and
+// error reporting.  Every entry point validates its arguments before any HIP
+// call; no entry point synchronises the host except emu_domain_status and
+// emu_release_workspace.
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+
+#include "../../include/emu.h"
+#include "emu_internal.h"
+
+namespace {
+
+using namespace emu;
+
+hipStream_t g_stream = nullptr;
+int g_split_mode = EMU_SPLIT_SYM;
+std::string g_err;
+
+// Workspace: [status word (offset 0), two FP64 split states (offset 128): 512 B]
+//            [operand A planes][operand B planes].
+// Grown only when a call needs more; the status word is preserved across growth.
+struct Workspace {
+    char *base = nullptr;
+    size_t bytes = 0;
+} g_ws;
+
+constexpr size_t HDR = 512;
+static_assert(128 + 2 * sizeof(F64SplitState) <= HDR, "workspace header");
+
+int fail(int code, const char *msg) {
+    g_err = msg;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+    g_err = std::string(what) + ": " + hipGetErrorString(e);
+    return EMU_EHIP;
+}
+
+size_t workspace_limit() {
+    const char *s = getenv("EMU_WORKSPACE_LIMIT");
+    if (!s || !*s) return (size_t)-1;
+    return (size_t)strtoull(s, nullptr, 0);
+}
+
+int ensure_workspace(size_t need) {
+    need += HDR;
+    if (need <= g_ws.bytes) return EMU_OK;
+    if (need > workspace_limit()) return fail(EMU_ENOMEM, "workspace would exceed EMU_WORKSPACE_LIMIT");
+    unsigned status = 0;
+    if (g_ws.base) {
+        hipError_t e = hipStreamSynchronize(g_stream);
+        if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+        e = hipMemcpy(&status, g_ws.base, sizeof(status), hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpy(status)");
+        e = hipFree(g_ws.base);
+        g_ws.base = nullptr;
+        g_ws.bytes = 0;
+        if (e != hipSuccess) return hip_fail(e, "hipFree");
+    }
+    void *p = nullptr;
+    hipError_t e = hipMalloc(&p, need);
+    if (e != hipSuccess || !p) {
+        (void)hipGetLastError();
+        return fail(EMU_ENOMEM, "hipMalloc of the workspace failed");
+    }
+    e = hipMemcpy(p, &status, sizeof(status), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(p);
+        return hip_fail(e, "hipMemcpy(status)");
+    }
+    e = hipMemset((char *)p + sizeof(status), 0, HDR - sizeof(status));
+    if (e != hipSuccess) {
+        (void)hipFree(p);
+        return hip_fail(e, "hipMemset(header)");
+    }
+    g_ws.base = (char *)p;
+    g_ws.bytes = need;
+    return EMU_OK;
+}
+
+unsigned *ws_status() { return reinterpret_cast<unsigned *>(g_ws.base); }
+F64SplitState *ws_states() { return reinterpret_cast<F64SplitState *>(g_ws.base + 128); }
+uint16_t *ws_planes(size_t off) { return reinterpret_cast<uint16_t *>(g_ws.base + HDR + off); }
+
+int nprod_to_d(int nprod) {
+    switch (nprod) {
+        case 6: return 3;
+        case 10: return 4;
+        case 15: return 5;
+        case 21: return 6;
+        default: return -1;
+    }
+}
+
+// Validation shared by both GEMMs (Sec. 3.2 problem statement, row-major).
+int check_gemm_args(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B,
+                    int64_t ldb, const void *C, int64_t ldc) {
+    if (M < 0 || N < 0 || K < 0) return fail(EMU_EINVAL, "M, N and K must be non-negative");
+    if (lda < (K > 1 ? K : 1)) return fail(EMU_EINVAL, "lda < max(1, K)");
+    if (ldb < (N > 1 ? N : 1)) return fail(EMU_EINVAL, "ldb < max(1, N)");
+    if (ldc < (N > 1 ? N : 1)) return fail(EMU_EINVAL, "ldc < max(1, N)");
+    if (M > 0 && N > 0 && !C) return fail(EMU_EINVAL, "C is NULL");
+    if (M > 0 && N > 0 && K > 0 && (!A || !B)) return fail(EMU_EINVAL, "A or B is NULL");
+    if (M > (int64_t)1 << 31 || N > (int64_t)1 << 31 || K > (int64_t)1 << 36)
+        return fail(EMU_EINVAL, "matrix dimension too large");
+    return EMU_OK;
+}
+
+struct Shape {
+    int64_t KB, RpadA, RpadB;
+    size_t bytesA, bytesB;
+};
+
+// Packed sizes: rows padded to whole GEMM tiles (tile_m, tile_n are multiples
+// of ROW_GROUP), reduction padded to whole k-blocks.
+Shape plan(int64_t M, int64_t N, int64_t K, int nplanes, int tile_m, int tile_n) {
+    Shape s;
+    s.KB = (K + KBLK - 1) / KBLK;
+    s.RpadA = round_up(M, tile_m);
+    s.RpadB = round_up(N, tile_n);
+    s.bytesA = (size_t)nplanes * s.KB * s.RpadA * KBLK * 2;
+    s.bytesB = (size_t)nplanes * s.KB * s.RpadB * KBLK * 2;
+    return s;
+}
+
+}  // namespace
+
+extern "C" {
+
+int emu_set_stream(void *hip_stream) {
+    g_stream = reinterpret_cast<hipStream_t>(hip_stream);
+    return EMU_OK;
+}
+
+int emu_set_split_mode(int mode) {
+    if (mode != EMU_SPLIT_SYM && mode != EMU_SPLIT_LITERAL)
+        return fail(EMU_EINVAL, "split mode must be EMU_SPLIT_SYM or EMU_SPLIT_LITERAL");
+    g_split_mode = mode;
+    return EMU_OK;
+}
+
+const char *emu_last_error(void) { return g_err.c_str(); }
+
+int64_t emu_workspace_bytes(void) { return (int64_t)g_ws.bytes; }
+
+int emu_release_workspace(void) {
+    if (!g_ws.base) return EMU_OK;
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+    e = hipFree(g_ws.base);
+    g_ws.base = nullptr;
+    g_ws.bytes = 0;
+    if (e != hipSuccess) return hip_fail(e, "hipFree");
+    return EMU_OK;
+}
+
+int emu_domain_status(unsigned *flags) {
+    if (!flags) return fail(EMU_EINVAL, "flags is NULL");
+    *flags = 0;
+    if (!g_ws.base) return EMU_OK;
+    hipError_t e = hipStreamSynchronize(g_stream);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    e = hipMemcpy(flags, g_ws.base, sizeof(unsigned), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy(status)");
+    const unsigned zero = 0;
+    e = hipMemcpy(g_ws.base, &zero, sizeof(unsigned), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy(status)");
+    return EMU_OK;
+}
+
+int emu_sgemm(int64_t M, int64_t N, int64_t K, const float *A, int64_t lda, const float *B,
+              int64_t ldb, float *C, int64_t ldc) {
+    int rc = check_gemm_args(M, N, K, A, lda, B, ldb, C, ldc);
+    if (rc) return rc;
+    g_err.clear();
+    if (M == 0 || N == 0) return EMU_OK;
+    if (K == 0) {
+        hipError_t e = launch_fill_f32(C, M, N, ldc, g_stream);
+        return e == hipSuccess ? EMU_OK : hip_fail(e, "fill");
+    }
+    const Shape s = plan(M, N, K, 3, SGEMM_MT, SGEMM_NT);
+    rc = ensure_workspace(s.bytesA + s.bytesB);
+    if (rc) return rc;
+    uint16_t *Ap = ws_planes(0), *Bp = ws_planes(s.bytesA);
+    hipError_t e = launch_split_f32(A, M, K, lda, false, Ap, s.KB, s.RpadA, ws_status(), g_stream);
+    if (e != hipSuccess) return hip_fail(e, "split_f32(A)");
+    e = launch_split_f32(B, K, N, ldb, true, Bp, s.KB, s.RpadB, ws_status(), g_stream);
+    if (e != hipSuccess) return hip_fail(e, "split_f32(B)");
+    e = launch_gemm_f32(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, g_stream);
+    if (e != hipSuccess) return hip_fail(e, "gemm_f32");
+    return EMU_OK;
+}
+
+int emu_dgemm(int64_t M, int64_t N, int64_t K, const double *A, int64_t lda, const double *B,
+              int64_t ldb, double *C, int64_t ldc, int nprod) {
+    const int d = nprod_to_d(nprod);
+    if (d < 0) return fail(EMU_EINVAL, "nprod must be 6, 10, 15 or 21");
+    int rc = check_gemm_args(M, N, K, A, lda, B, ldb, C, ldc);
+    if (rc) return rc;
+    g_err.clear();
+    if (M == 0 || N == 0) return EMU_OK;
+    if (K == 0) {
+        hipError_t e = launch_fill_f64(C, M, N, ldc, g_stream);
+        return e == hipSuccess ? EMU_OK : hip_fail(e, "fill");
+    }
+    // Only the d slices the retained products read are materialised; the
+    // levels after them never influence slices 0 .. d-1.
+    const Shape s = plan(M, N, K, d, dgemm_mt(d), DGEMM_NT);
+    rc = ensure_workspace(s.bytesA + s.bytesB);
+    if (rc) return rc;
+    uint16_t *Ap = ws_planes(0), *Bp = ws_planes(s.bytesA);
+    F64SplitState *st = ws_states();
+    hipError_t e = launch_split_f64(A, M, K, lda, false, Ap, s.KB, s.RpadA, d, g_split_mode, st,
+                                    ws_status(), g_stream);
+    if (e != hipSuccess) return hip_fail(e, "split_f64(A)");
+    e = launch_split_f64(B, K, N, ldb, true, Bp, s.KB, s.RpadB, d, g_split_mode, st + 1,
+                         ws_status(), g_stream);
+    if (e != hipSuccess) return hip_fail(e, "split_f64(B)");
+    e = launch_gemm_f64(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, d, g_stream);
+    if (e != hipSuccess) return hip_fail(e, "gemm_f64");
+    return EMU_OK;
+}
+
+static int check_split_args(int64_t R, int64_t Cc, const void *X, int64_t ldx, int as_b,
+                            const void *out) {
+    if (R < 0 || Cc < 0) return fail(EMU_EINVAL, "R and Cc must be non-negative");
+    if (ldx < (Cc > 1 ? Cc : 1)) return fail(EMU_EINVAL, "ldx < max(1, Cc)");
+    if (as_b != 0 && as_b != 1) return fail(EMU_EINVAL, "as_b must be 0 or 1");
+    if (R > 0 && Cc > 0 && (!X || !out)) return fail(EMU_EINVAL, "NULL pointer");
+    return EMU_OK;
+}
+
+int emu_split_f32(int64_t R, int64_t Cc, const float *X, int64_t ldx, int as_b, uint16_t *comps) {
+    int rc = check_split_args(R, Cc, X, ldx, as_b, comps);
+    if (rc) return rc;
+    g_err.clear();
+    if (R == 0 || Cc == 0) return EMU_OK;
+    const int64_t rows = as_b ? Cc : R, K = as_b ? R : Cc;   // packed rows and reduction length
+    const Shape s = plan(rows, 1, K, 3, ROW_GROUP, ROW_GROUP);
+    rc = ensure_workspace(s.bytesA);
+    if (rc) return rc;
+    uint16_t *P = ws_planes(0);
+    hipError_t e = launch_split_f32(X, R, Cc, ldx, as_b != 0, P, s.KB, s.RpadA, ws_status(),
+                                    g_stream);
+    if (e != hipSuccess) return hip_fail(e, "split_f32");
+    e = launch_unpack(P, 3, s.KB, s.RpadA, R, Cc, as_b != 0, comps, g_stream);
+    if (e != hipSuccess) return hip_fail(e, "unpack");
+    return EMU_OK;
+}
+
+int emu_split_f64(int64_t R, int64_t Cc, const double *X, int64_t ldx, int as_b,
+                  uint16_t *slices, int32_t *v) {
+    int rc = check_split_args(R, Cc, X, ldx, as_b, slices);
+    if (rc) return rc;
+    if (!v) return fail(EMU_EINVAL, "v is NULL");
+    g_err.clear();
+    const int64_t rows = as_b ? Cc : R, K = as_b ? R : Cc;
+    const Shape s = plan(rows, 1, K, 6, ROW_GROUP, ROW_GROUP);
+    rc = ensure_workspace(s.bytesA > 0 ? s.bytesA : 1);
+    if (rc) return rc;
+    uint16_t *P = ws_planes(0);
+    F64SplitState *st = ws_states();
+    hipError_t e = launch_split_f64(X, R, Cc, ldx, as_b != 0, P, s.KB, s.RpadA, 6, g_split_mode, st,
+                                    ws_status(), g_stream);
+    if (e != hipSuccess) return hip_fail(e, "split_f64");
+    if (R > 0 && Cc > 0) {
+        e = launch_unpack(P, 6, s.KB, s.RpadA, R, Cc, as_b != 0, slices, g_stream);
+        if (e != hipSuccess) return hip_fail(e, "unpack");
+    }
+    e = launch_copy_v(st, v, g_stream);
+    if (e != hipSuccess) return hip_fail(e, "copy_v");
+    return EMU_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,85 @@
+// Internal definitions shared by the HIP kernels and the host library.
+//
+// Packed operand format (the bf16 MFMA operand layout written by the split
+// kernels and read by the GEMM kernels).  An operand is viewed as R "rows" by
+// K reduction indices: for A the rows are A's rows; for B (K x N) the rows are
+// B's columns, i.e. B is stored transposed so that every row is K-contiguous.
+//
+//   element (c, row, k) of component plane c lives at bf16 index
+//     ((c * KB + kb) * Rpad + row) * 32 + 8 * (q ^ swz(row)) + (k % 8)
+//   with kb = k / 32, q = (k % 32) / 8, swz(row) = (row >> 1) & 3,
+//   KB = ceil(K / 32), Rpad = R rounded up to a multiple of 64 and of the
+//   GEMM tile extent along the rows.
+//
+// So one k-block of a component is a row-major [Rpad][32] bf16 slab, 64 bytes
+// per row: a workgroup tile of T rows is one contiguous T*64-byte block that a
+// direct global->LDS copy moves as is.  The 16-byte chunks inside a row are
+// XOR-swizzled by bits 1..2 of the row so that the MFMA operand reads of 32
+// consecutive rows (one 16-byte chunk each, ds_read_b128) hit distinct LDS
+// bank groups within every group of eight lanes.  Padding rows and k >= K are
+// zero.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace emu {
+
+constexpr int KBLK = 32;        // reduction indices per k-block (one LDS stage)
+constexpr int ROW_GROUP = 64;   // packed rows are padded to a multiple of this ...
+constexpr int KPANEL = 256;     // reduction panel B_K of the FP32/FP64 reconstruction
+
+// ... and of the GEMM tile that reads them (output tile rows for A, columns for B).
+constexpr int SGEMM_MT = 192, SGEMM_NT = 128;
+constexpr int DGEMM_NT = 64;
+inline int dgemm_mt(int d) { return d <= 4 ? 128 : 64; }
+constexpr int KB_PER_PANEL = KPANEL / KBLK;
+
+__host__ __device__ inline int swz(int64_t row) { return (int)((row >> 1) & 3); }
+
+__host__ __device__ inline int64_t packed_index(int c, int64_t kb, int64_t row, int q, int64_t KB,
+                                                int64_t Rpad) {
+    return ((c * KB + kb) * Rpad + row) * KBLK + 8 * (q ^ swz(row));
+}
+
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// Status bits (same values as EMU_STATUS_* in emu.h).
+constexpr unsigned ST_NAN = 1u, ST_RANGE = 2u, ST_SUBNORMAL = 4u, ST_OVERFLOW = 8u;
+
+// Device state of one FP64 operand split: the operand-wide per-level maxima
+// (bit patterns of non-negative doubles, whose unsigned order is the numeric
+// order), the exponent chain v, and the first level a replay pass must
+// recompute (-1 when the chain is verified).
+struct alignas(64) F64SplitState {
+    unsigned long long maxbits[6];
+    int v[6];
+    int replay_from;
+    int nlev;
+    int mode;
+    int pad[3];
+};
+
+constexpr int V_ZERO = (int)0x80000000;   // level whose residual is identically zero
+
+}  // namespace emu
+
+// Launch wrappers (defined in the .hip files, called by the host API).
+namespace emu {
+hipError_t launch_fill_f32(float *C, int64_t M, int64_t N, int64_t ldc, hipStream_t s);
+hipError_t launch_fill_f64(double *C, int64_t M, int64_t N, int64_t ldc, hipStream_t s);
+hipError_t launch_split_f32(const float *X, int64_t rows, int64_t cols, int64_t ldx, bool as_b,
+                            uint16_t *P, int64_t KB, int64_t Rpad, unsigned *status,
+                            hipStream_t s);
+hipError_t launch_split_f64(const double *X, int64_t rows, int64_t cols, int64_t ldx, bool as_b,
+                            uint16_t *P, int64_t KB, int64_t Rpad, int nlev, int mode,
+                            F64SplitState *st, unsigned *status, hipStream_t s);
+hipError_t launch_unpack(const uint16_t *P, int nc, int64_t KB, int64_t Rpad, int64_t rows,
+                         int64_t cols, bool as_b, uint16_t *out, hipStream_t s);
+hipError_t launch_copy_v(const F64SplitState *st, int32_t *v, hipStream_t s);
+hipError_t launch_gemm_f32(const uint16_t *Ap, const uint16_t *Bp, float *C, int64_t M, int64_t N,
+                           int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc, hipStream_t s);
+hipError_t launch_gemm_f64(const uint16_t *Ap, const uint16_t *Bp, double *C, int64_t M,
+                           int64_t N, int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc,
+                           int d, hipStream_t s);
+}  // namespace emu

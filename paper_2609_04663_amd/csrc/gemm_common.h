@@ -1,0 +1,57 @@
+// Device helpers shared by the multi-product GEMM kernels.
+#pragma once
+
+#include "emu_internal.h"
+
+namespace emu {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void *lds_void_ptr;
+
+// Workgroup -> output tile.  The hardware hands workgroup i to XCD i % 8; the
+// remap gives each XCD a contiguous run of tile ids, and tile ids walk the
+// output in groups of GROUP_M tile-rows so that the workgroups resident on one
+// XCD at a time share A row-panels and B column-panels in that XCD's L2.
+template <int GROUP_M>
+__device__ inline void tile_coords(int nt_m, int nt_n, int &tm, int &tn) {
+    const int nwg = gridDim.x, w = blockIdx.x;
+    const int per = nwg / 8, rem = nwg % 8, x = w % 8, j = w / 8;
+    const int id = (x < rem) ? x * (per + 1) + j : rem * (per + 1) + (x - rem) * per + j;
+    const int group = GROUP_M * nt_n;
+    const int g = id / group, first = g * GROUP_M;
+    const int gm = min(nt_m - first, GROUP_M);
+    const int r = id - g * group;
+    tm = first + r % gm;
+    tn = r / gm;
+}
+
+// One 1 KB direct global->LDS copy by a wave: lane l moves 16 bytes from
+// src + 16 l to lds_dst + 16 l (lds_dst must be uniform over the wave).
+__device__ inline void copy_1k(const char *src_wave, char *lds_dst, int lane) {
+    __builtin_amdgcn_global_load_lds((const void *)(src_wave + lane * 16), (lds_void_ptr)lds_dst, 16,
+                                     0, 0);
+}
+
+// Per-lane byte offset, inside a [rows][64 B] LDS tile, of the MFMA operand
+// fragment of a 32-row block for reduction sub-step s (16 indices): lane l
+// reads row (l % 32), 16-byte chunk q = 2 s + l / 32, swizzled as packed.
+__device__ inline int frag_offset(int lane, int s) {
+    const int row = lane & 31;
+    const int q = 2 * s + (lane >> 5);
+    return row * 64 + ((q ^ ((row >> 1) & 3)) << 4);
+}
+
+__device__ inline bf16x8 lds_frag(const char *tile_block, int off) {
+    return *reinterpret_cast<const bf16x8 *>(tile_block + off);
+}
+
+__device__ inline f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Output coordinates of accumulator register r of lane l in a 32x32 block:
+// row (r / 4) * 8 + (l / 32) * 4 + r % 4, column l % 32.
+__device__ inline int acc_row(int lane, int r) { return (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3); }
+
+}  // namespace emu

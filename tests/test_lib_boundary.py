@@ -1,0 +1,91 @@
+"""CPU-side checks of the C-ABI library (no kernel is launched).
+
+The library must load, export every function include/emu.h declares, and
+reject invalid arguments with EMU_EINVAL before touching the HIP runtime.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+LIB = os.path.join(ROOT, "paper_2609_04663_amd", "libemu.so")
+
+
+def _declared():
+    with open(os.path.join(ROOT, "include", "emu.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w\s\*]+?\b(emu_\w+)\s*\(", text, re.M)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(LIB):
+        pytest.fail("libemu.so is not built (run __graft_entry__.build())")
+    import paper_2609_04663_amd as emu
+    return emu.lib()
+
+
+def test_header_declares_the_paper_entry_points():
+    names = _declared()
+    for n in ("emu_sgemm", "emu_dgemm", "emu_set_stream", "emu_domain_status",
+              "emu_last_error", "emu_release_workspace", "emu_split_f32", "emu_split_f64"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(L):
+    import paper_2609_04663_amd as emu
+    for n in _declared():
+        assert hasattr(L, n), n
+    assert set(emu.EXPORTS) == set(_declared())
+
+
+P = ctypes.c_void_p(0x1000)     # never dereferenced: validation fails first
+
+
+@pytest.mark.parametrize("args", [
+    (-1, 4, 4, P, 4, P, 4, P, 4),        # negative M
+    (4, -1, 4, P, 4, P, 4, P, 4),        # negative N
+    (4, 4, -1, P, 4, P, 4, P, 4),        # negative K
+    (4, 4, 8, P, 7, P, 4, P, 4),         # lda < K
+    (4, 8, 4, P, 4, P, 7, P, 8),         # ldb < N
+    (4, 8, 4, P, 4, P, 8, P, 7),         # ldc < N
+    (4, 4, 4, None, 4, P, 4, P, 4),      # NULL A
+    (4, 4, 4, P, 4, None, 4, P, 4),      # NULL B
+    (4, 4, 4, P, 4, P, 4, None, 4),      # NULL C
+])
+def test_gemm_invalid_arguments(L, args):
+    import paper_2609_04663_amd as emu
+    assert L.emu_sgemm(*args) == emu.EMU_EINVAL
+    assert L.emu_last_error()
+    assert L.emu_dgemm(*args, 10) == emu.EMU_EINVAL
+
+
+@pytest.mark.parametrize("nprod", [0, 1, 3, 7, 20, 36, -6])
+def test_dgemm_invalid_nprod(L, nprod):
+    import paper_2609_04663_amd as emu
+    assert L.emu_dgemm(4, 4, 4, P, 4, P, 4, P, 4, nprod) == emu.EMU_EINVAL
+
+
+def test_empty_output_is_a_no_op(L):
+    import paper_2609_04663_amd as emu
+    assert L.emu_sgemm(0, 4, 4, P, 4, P, 4, P, 4) == emu.EMU_OK
+    assert L.emu_dgemm(4, 0, 4, P, 4, P, 1, P, 1, 6) == emu.EMU_OK
+
+
+def test_split_hooks_invalid(L):
+    import paper_2609_04663_amd as emu
+    assert L.emu_split_f32(-1, 4, P, 4, 0, P) == emu.EMU_EINVAL
+    assert L.emu_split_f32(4, 4, P, 3, 0, P) == emu.EMU_EINVAL
+    assert L.emu_split_f32(4, 4, P, 4, 2, P) == emu.EMU_EINVAL
+    assert L.emu_split_f64(4, 4, P, 4, 0, P, None) == emu.EMU_EINVAL
+
+
+def test_split_mode_and_status_arguments(L):
+    import paper_2609_04663_amd as emu
+    assert L.emu_set_split_mode(2) == emu.EMU_EINVAL
+    assert L.emu_set_split_mode(emu.SPLIT_LITERAL) == emu.EMU_OK
+    assert L.emu_set_split_mode(emu.SPLIT_SYM) == emu.EMU_OK
+    assert L.emu_domain_status(None) == emu.EMU_EINVAL
+    assert L.emu_set_stream(None) == emu.EMU_OK
