@@ -1,0 +1,220 @@
+#!/usr/bin/env python3
+"""Benchmark of FP32/FP64 GEMM emulated through BF16 component products on
+one MI355X: effective TFLOP/s (2MNK / t) of emu-SGEMM and emu-DGEMM for every
+product count, with the bf16 MFMA roofline fraction of the product GEMMs.
+
+One step = one pass of the whole hot path at M = N = K = 8192:
+  emu_sgemm (3 BF16 components, 6 products; standard-normal FP32 inputs), then
+  emu_dgemm with nprod = 6, 10, 15, 21 (six-slice split; wide-range FP64 inputs
+  s * m * 2^e, m uniform in [1, 2), e uniform integer in [-20, 20]).
+Each call includes its split/pack kernels, its GEMM kernel and its FP64
+reconstruction, exactly as the library runs them; inputs are resident in HBM
+before the timed region.
+
+Prints one JSON line.  Also reported: per-variant phase times from HIP events
+recorded by the library on its stream (split/pack vs GEMM, the analog of the
+paper's runtime breakdown), the roofline object of the dominant kernel, a
+sampled parity check against the CPU oracle, and the oracle itself timed on the
+host cores as a baseline.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA (AMD published)
+PEAK_FP32_MATRIX = 157.3       # context: native FP32 matrix
+PEAK_FP64_MATRIX = 78.6        # context: native FP64 matrix/vector
+VARIANTS = [("sgemm", 6), ("dgemm", 6), ("dgemm", 10), ("dgemm", 15), ("dgemm", 21)]
+KERNEL_SOURCES = {
+    "sgemm": "paper_2609_04663_amd/csrc/gemm_f32.hip",
+    "dgemm": "paper_2609_04663_amd/csrc/gemm_f64.hip",
+}
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def source_hash(rel):
+    with open(os.path.join(ROOT, rel), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def traffic_for(kernel_key):
+    """HBM bytes per launch from the committed rocprofv3 PMC summary, if it was
+    taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    e = t.get(kernel_key)
+    if not e:
+        return None
+    src = KERNEL_SOURCES[kernel_key.split(":")[0]]
+    if e.get("source_sha256_16") != source_hash(src):
+        return None
+    return e.get("bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--size", type=int, default=8192, help="M = N = K")
+    ap.add_argument("--cpu-rows", type=int, default=2,
+                    help="rows of C the oracle computes per variant for the CPU baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(how the computation would shard is described in DESIGN.md).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_04663_amd as emu
+    import seeded_inputs as S
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    n = args.size
+    log(f"bench: generating inputs M=N=K={n}")
+    sa, sb = S.seeds(2)
+    A32 = S.make("normal", sa, (n, n), np.float32)
+    B32 = S.make("normal", sb, (n, n), np.float32)
+    da, db = S.seeds(4)
+    A64 = S.make("wide", da, (n, n), np.float64)
+    B64 = S.make("wide", db, (n, n), np.float64)
+    dA32, dB32 = torch.from_numpy(A32).cuda(), torch.from_numpy(B32).cuda()
+    dA64, dB64 = torch.from_numpy(A64).cuda(), torch.from_numpy(B64).cuda()
+    C32 = torch.empty((n, n), dtype=torch.float32, device="cuda")
+    C64 = {p: torch.empty((n, n), dtype=torch.float64, device="cuda") for p in (6, 10, 15, 21)}
+
+    def step():
+        emu.sgemm(dA32, dB32, C=C32)
+        for p in (6, 10, 15, 21):
+            emu.dgemm(dA64, dB64, p, C=C64[p])
+
+    log(f"bench: warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    emu.domain_status()
+    emu.profile_enable(True)
+    emu.profile_read()
+    torch.cuda.synchronize()
+    log(f"bench: timing {args.steps} steps")
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    split_ms, gemm_ms = emu.profile_read()
+    emu.profile_enable(False)
+    status = emu.domain_status()
+    assert len(split_ms) == len(VARIANTS) * args.steps, "profile pool too small"
+
+    flop = 2.0 * n ** 3
+    elapsed = t1 - t0
+    value = len(VARIANTS) * flop * args.steps / elapsed / 1e12
+    per_variant = {}
+    for vi, (kind, p) in enumerate(VARIANTS):
+        s = np.array(split_ms[vi::len(VARIANTS)])
+        g = np.array(gemm_ms[vi::len(VARIANTS)])
+        name = "emu-SGEMM" if kind == "sgemm" else f"emu-DGEMM-{p}"
+        per_variant[name] = {
+            "effective_tflops": round(flop / ((s.mean() + g.mean()) * 1e-3) / 1e12, 2),
+            "split_ms": round(float(s.mean()), 4),
+            "gemm_ms": round(float(g.mean()), 4),
+            "split_share": round(float(s.mean() / (s.mean() + g.mean())), 4),
+            "mfma_frac": round(p * flop / (g.mean() * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        }
+    # dominant kernel: the GEMM launch with the largest share of the step
+    dom = max(range(len(VARIANTS)), key=lambda i: np.mean(gemm_ms[i::len(VARIANTS)]))
+    kind, p = VARIANTS[dom]
+    g_avg = float(np.mean(gemm_ms[dom::len(VARIANTS)]))
+    achieved = p * flop / (g_avg * 1e-3) / 1e12
+    kkey = f"{kind}:{p}:{n}"
+    roofline = {
+        "kernel": ("gemm_f32_kernel" if kind == "sgemm" else f"gemm_f64_kernel<d={ {6: 3, 10: 4, 15: 5, 21: 6}[p]}>"),
+        "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+        "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+        "traffic": traffic_for(kkey),
+        "per_launch": f"{p} x 2MNK bf16 MFMA flops / mean HIP-event time of the GEMM launch",
+    }
+
+    # sampled parity of this very run against the oracle, and the oracle timing
+    cpu = None
+    parity = None
+    if not args.no_cpu_baseline and args.cpu_rows > 0:
+        import oracle as O
+        rows = np.repeat(np.arange(args.cpu_rows, dtype=np.int64), n)
+        cols = np.tile(np.arange(n, dtype=np.int64), args.cpu_rows)
+        got32 = C32[: args.cpu_rows].cpu().numpy().ravel()
+        log(f"bench: oracle on {args.cpu_rows} rows per variant ({O.num_threads()} threads)")
+        tc0 = time.perf_counter()
+        orc32, _ = O.emu_sgemm_entries(A32, B32, rows, cols)
+        t_s = time.perf_counter() - tc0
+        ref = (A32[: args.cpu_rows].astype(np.float64) @ B32.astype(np.float64)).ravel()
+        e_gpu = float(np.linalg.norm(got32 - ref) / np.linalg.norm(ref))
+        e_orc = float(np.linalg.norm(orc32 - ref) / np.linalg.norm(ref))
+        parity = {"sgemm_rows_eF_gpu": e_gpu, "sgemm_rows_eF_oracle": e_orc}
+        t_total = t_s
+        bitexact = {}
+        for p in (6, 10, 15, 21):
+            tc0 = time.perf_counter()
+            orc64, _ = O.emu_dgemm_entries(A64, B64, rows, cols, p)
+            t_total += time.perf_counter() - tc0
+            got64 = C64[p][: args.cpu_rows].cpu().numpy().ravel()
+            bitexact[str(p)] = bool(np.array_equal(got64, orc64))
+        parity["dgemm_rows_bitexact"] = bitexact
+        cpu = {
+            "value": round(len(VARIANTS) * 2.0 * n * rows.size / t_total / 1e12, 6),
+            "unit": "effective TFLOP/s",
+            "cores": O.num_threads(),
+            "kind": "oracle",
+            "sample": (f"rows 0..{args.cpu_rows - 1} of C ({rows.size} entries) for each of the 5 "
+                       f"variants at M=N=K={n}, each call including the oracle's split of the "
+                       f"full operands; {t_total:.1f} s"),
+        }
+
+    line = {
+        "metric": "effective TFLOP/s (2MNK/t) emu-SGEMM & emu-DGEMM per nprod; % bf16 MFMA peak",
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"M=N=K={n}: emu-SGEMM (3 comps, 6 products, standard-normal FP32) + "
+                         f"emu-DGEMM nprod 6/10/15/21 (six slices, FP64 s*m*2^e, e in [-20,20])"),
+            "M": n, "N": n, "K": n, "calls_per_step": len(VARIANTS),
+        },
+        "per_variant": per_variant,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "parity": parity,
+        "domain_status": status,
+        "context_peaks_tflops": {"bf16_mfma": PEAK_BF16_TFLOPS, "fp32_matrix": PEAK_FP32_MATRIX,
+                                 "fp64_matrix": PEAK_FP64_MATRIX},
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

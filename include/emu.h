@@ -127,6 +127,22 @@ int emu_split_f32(int64_t R, int64_t Cc, const float *X, int64_t ldx, int as_b, 
 int emu_split_f64(int64_t R, int64_t Cc, const double *X, int64_t ldx, int as_b,
                   uint16_t *slices, int32_t *v);
 
+/* Phase timing, the analog of the paper's runtime breakdown (Sec. 8.4):
+   decomposition + packing versus the component-product GEMM with its
+   reconstruction.  emu_profile_enable(1) creates a pool of HIP events for
+   4096 calls (the only allocation, done here, outside any timed region); from
+   then on every emu_sgemm / emu_dgemm records three events on its stream:
+   before its split kernels, between them and its GEMM kernel, and after the
+   GEMM kernel.  emu_profile_read synchronises the device, writes the split/pack
+   and GEMM milliseconds of the profiled calls since the previous read, oldest
+   first, into split_ms[i] and gemm_ms[i] for i < min(cap, *calls) (host arrays
+   owned by the caller), stores the number of such calls in *calls and starts
+   over.  Calls made while the pool is full are not profiled.
+   emu_profile_enable(0) destroys the pool.  EMU_EINVAL if calls is NULL, or if
+   cap > 0 and an array is NULL. */
+int emu_profile_enable(int on);
+int emu_profile_read(int64_t cap, double *split_ms, double *gemm_ms, int64_t *calls);
+
 #ifdef __cplusplus
 }
 #endif

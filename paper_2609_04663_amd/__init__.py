@@ -30,7 +30,8 @@ NPROD = (6, 10, 15, 21)
 
 EXPORTS = ("emu_sgemm", "emu_dgemm", "emu_set_stream", "emu_set_split_mode",
            "emu_domain_status", "emu_last_error", "emu_release_workspace",
-           "emu_workspace_bytes", "emu_split_f32", "emu_split_f64")
+           "emu_workspace_bytes", "emu_split_f32", "emu_split_f64", "emu_profile_enable",
+           "emu_profile_read")
 
 
 class EmuError(RuntimeError):
@@ -60,9 +61,11 @@ def lib() -> ctypes.CDLL:
         L.emu_workspace_bytes.restype = i64
         L.emu_split_f32.argtypes = [i64, i64, p, i64, ci, p]
         L.emu_split_f64.argtypes = [i64, i64, p, i64, ci, p, p]
+        L.emu_profile_enable.argtypes = [ci]
+        L.emu_profile_read.argtypes = [i64, p, p, ctypes.POINTER(ctypes.c_int64)]
         for name in ("emu_sgemm", "emu_dgemm", "emu_set_stream", "emu_set_split_mode",
                      "emu_domain_status", "emu_release_workspace", "emu_split_f32",
-                     "emu_split_f64"):
+                     "emu_split_f64", "emu_profile_enable", "emu_profile_read"):
             getattr(L, name).restype = ci
         _lib = L
     return _lib
@@ -152,6 +155,22 @@ def domain_status() -> int:
     f = ctypes.c_uint(0)
     _check(lib().emu_domain_status(ctypes.byref(f)))
     return int(f.value)
+
+
+def profile_enable(on: bool = True):
+    """Record split/pack and GEMM phase times of every call (see emu.h)."""
+    _check(lib().emu_profile_enable(int(on)))
+
+
+def profile_read(cap: int = 4096):
+    """Per-call (split_ms, gemm_ms) lists of the profiled calls since the last
+    read, oldest first; synchronises."""
+    s = (ctypes.c_double * cap)()
+    g = (ctypes.c_double * cap)()
+    n = ctypes.c_int64()
+    _check(lib().emu_profile_read(cap, s, g, ctypes.byref(n)))
+    k = min(cap, int(n.value))
+    return list(s[:k]), list(g[:k])
 
 
 def release_workspace():

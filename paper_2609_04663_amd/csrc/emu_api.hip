@@ -7,6 +7,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <string>
+#include <vector>
 
 #include "../../include/emu.h"
 #include "emu_internal.h"
@@ -80,6 +81,27 @@ int ensure_workspace(size_t need) {
     g_ws.base = (char *)p;
     g_ws.bytes = need;
     return EMU_OK;
+}
+
+// Phase profiling: a fixed pool of event triples, created by emu_profile_enable.
+struct Profile {
+    bool on = false;
+    std::vector<hipEvent_t> ev;     // 3 per call
+    size_t used = 0;                // triples used since the last read
+} g_prof;
+
+constexpr size_t PROFILE_CALLS = 4096;
+
+// Event slot of the current call's phase boundary p (0, 1, 2), or null.
+hipEvent_t prof_event(int p) {
+    if (!g_prof.on || g_prof.used >= PROFILE_CALLS) return nullptr;
+    return g_prof.ev[3 * g_prof.used + p];
+}
+
+void prof_mark(int p) {
+    hipEvent_t e = prof_event(p);
+    if (e) (void)hipEventRecord(e, g_stream);
+    if (e && p == 2) ++g_prof.used;
 }
 
 unsigned *ws_status() { return reinterpret_cast<unsigned *>(g_ws.base); }
@@ -158,6 +180,47 @@ int emu_release_workspace(void) {
     return EMU_OK;
 }
 
+int emu_profile_enable(int on) {
+    if (on && !g_prof.on) {
+        g_prof.ev.assign(3 * PROFILE_CALLS, nullptr);
+        for (auto &e : g_prof.ev) {
+            hipError_t r = hipEventCreate(&e);
+            if (r != hipSuccess) return hip_fail(r, "hipEventCreate");
+        }
+        g_prof.used = 0;
+        g_prof.on = true;
+    } else if (!on && g_prof.on) {
+        (void)hipDeviceSynchronize();
+        for (auto &e : g_prof.ev)
+            if (e) (void)hipEventDestroy(e);
+        g_prof.ev.clear();
+        g_prof.used = 0;
+        g_prof.on = false;
+    }
+    return EMU_OK;
+}
+
+int emu_profile_read(int64_t cap, double *split_ms, double *gemm_ms, int64_t *calls) {
+    if (!calls || (cap > 0 && (!split_ms || !gemm_ms)))
+        return fail(EMU_EINVAL, "NULL output pointer");
+    *calls = 0;
+    if (!g_prof.on) return EMU_OK;
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+    for (size_t i = 0; i < g_prof.used && (int64_t)i < cap; ++i) {
+        float a = 0.f, b = 0.f;
+        e = hipEventElapsedTime(&a, g_prof.ev[3 * i], g_prof.ev[3 * i + 1]);
+        if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+        e = hipEventElapsedTime(&b, g_prof.ev[3 * i + 1], g_prof.ev[3 * i + 2]);
+        if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+        split_ms[i] = a;
+        gemm_ms[i] = b;
+    }
+    *calls = (int64_t)g_prof.used;
+    g_prof.used = 0;
+    return EMU_OK;
+}
+
 int emu_domain_status(unsigned *flags) {
     if (!flags) return fail(EMU_EINVAL, "flags is NULL");
     *flags = 0;
@@ -186,12 +249,15 @@ int emu_sgemm(int64_t M, int64_t N, int64_t K, const float *A, int64_t lda, cons
     rc = ensure_workspace(s.bytesA + s.bytesB);
     if (rc) return rc;
     uint16_t *Ap = ws_planes(0), *Bp = ws_planes(s.bytesA);
+    prof_mark(0);
     hipError_t e = launch_split_f32(A, M, K, lda, false, Ap, s.KB, s.RpadA, ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f32(A)");
     e = launch_split_f32(B, K, N, ldb, true, Bp, s.KB, s.RpadB, ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f32(B)");
+    prof_mark(1);
     e = launch_gemm_f32(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, g_stream);
     if (e != hipSuccess) return hip_fail(e, "gemm_f32");
+    prof_mark(2);
     return EMU_OK;
 }
 
@@ -214,14 +280,17 @@ int emu_dgemm(int64_t M, int64_t N, int64_t K, const double *A, int64_t lda, con
     if (rc) return rc;
     uint16_t *Ap = ws_planes(0), *Bp = ws_planes(s.bytesA);
     F64SplitState *st = ws_states();
+    prof_mark(0);
     hipError_t e = launch_split_f64(A, M, K, lda, false, Ap, s.KB, s.RpadA, d, g_split_mode, st,
                                     ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f64(A)");
     e = launch_split_f64(B, K, N, ldb, true, Bp, s.KB, s.RpadB, d, g_split_mode, st + 1,
                          ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f64(B)");
+    prof_mark(1);
     e = launch_gemm_f64(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, d, g_stream);
     if (e != hipSuccess) return hip_fail(e, "gemm_f64");
+    prof_mark(2);
     return EMU_OK;
 }
 

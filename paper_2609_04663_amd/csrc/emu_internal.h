@@ -32,7 +32,7 @@ constexpr int KPANEL = 256;     // reduction panel B_K of the FP32/FP64 reconstr
 // ... and of the GEMM tile that reads them (output tile rows for A, columns for B).
 constexpr int SGEMM_MT = 192, SGEMM_NT = 128;
 constexpr int DGEMM_NT = 64;
-inline int dgemm_mt(int d) { return d <= 4 ? 128 : 64; }
+inline int dgemm_mt(int d) { return d == 3 ? 128 : 64; }
 constexpr int KB_PER_PANEL = KPANEL / KBLK;
 
 __host__ __device__ inline int swz(int64_t row) { return (int)((row >> 1) & 3); }

@@ -35,18 +35,6 @@ struct Cfg {
     static_assert(2 * STAGE <= 160 * 1024, "LDS");
 };
 
-// Product q of the executed order: diagonal l ascending, i ascending.
-__host__ __device__ constexpr int prod_i(int q) {
-    int l = 0;
-    while (q > l) { q -= l + 1; ++l; }
-    return q;
-}
-__host__ __device__ constexpr int prod_j(int q) {
-    int l = 0;
-    while (q > l) { q -= l + 1; ++l; }
-    return l - q;
-}
-
 template <int D, int BM>
 __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
     const uint16_t *__restrict__ Ap, const uint16_t *__restrict__ Bp, double *__restrict__ C,
@@ -110,11 +98,16 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
 #pragma unroll
                 for (int b = 0; b < BM; ++b) af[c][b] = lds_frag(At + c * K::A_BYTES + b * 32 * 64, off);
             }
+            // product q = l (l + 1) / 2 + i is A_i B_(l - i): diagonal l ascending,
+            // i ascending (all indices are compile-time constants after unrolling)
 #pragma unroll
-            for (int q = 0; q < K::P; ++q)
+            for (int l = 0; l < D; ++l)
 #pragma unroll
-                for (int b = 0; b < BM; ++b)
-                    acc[q][b] = mfma(af[prod_i(q)][b], bf[prod_j(q)], acc[q][b]);
+                for (int i = 0; i <= l; ++i)
+#pragma unroll
+                    for (int b = 0; b < BM; ++b)
+                        acc[l * (l + 1) / 2 + i][b] =
+                            mfma(af[i][b], bf[l - i], acc[l * (l + 1) / 2 + i][b]);
         }
     };
 
@@ -170,7 +163,7 @@ hipError_t launch_gemm_f64(const uint16_t *Ap, const uint16_t *Bp, double *C, in
                            int d, hipStream_t s) {
     switch (d) {
         case 3: return launch_t<3, 2>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, s);
-        case 4: return launch_t<4, 2>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, s);   // MT = dgemm_mt(d)
+        case 4: return launch_t<4, 1>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, s);
         case 5: return launch_t<5, 1>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, s);
         case 6: return launch_t<6, 1>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, s);
         default: return hipErrorInvalidValue;
