@@ -66,83 +66,82 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
         }
     };
 
-    f32x16 hi[RB][2], lo[RB][2], blk[RB][2];
+    const int off0 = frag_offset(lane, 0), off1 = frag_offset(lane, 1);
+
+    // One 16-index sub-step on the stage at `base`: 36 MFMAs into hi / lo.
+    auto substep = [&](const char *base, int off, f32x16 (&hi)[RB][2], f32x16 (&lo)[RB][2]) {
+        const char *At = base + (wm * 32 * RB) * 64;
+        const char *Bt = base + NC * A_BYTES + (wn * 64) * 64;
+        bf16x8 bfr[NC][2];
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb) bfr[c][cb] = lds_frag(Bt + c * B_BYTES + cb * 32 * 64, off);
+        bf16x8 afr[RB];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) afr[rb] = lds_frag(At + rb * 32 * 64, off);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb) hi[rb][cb] = mfma(afr[rb], bfr[0][cb], hi[rb][cb]);
+#pragma unroll
+        for (int j = 1; j < 3; ++j)
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb) lo[rb][cb] = mfma(afr[rb], bfr[j][cb], lo[rb][cb]);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) afr[rb] = lds_frag(At + A_BYTES + rb * 32 * 64, off);
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb) lo[rb][cb] = mfma(afr[rb], bfr[j][cb], lo[rb][cb]);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) afr[rb] = lds_frag(At + 2 * A_BYTES + rb * 32 * 64, off);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb) lo[rb][cb] = mfma(afr[rb], bfr[0][cb], lo[rb][cb]);
+    };
+
+    f32x16 blk[RB][2];
 #pragma unroll
     for (int i = 0; i < RB; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            hi[i][j] = f32x16{};
-            lo[i][j] = f32x16{};
-            blk[i][j] = f32x16{};
-        }
+        for (int j = 0; j < 2; ++j) blk[i][j] = f32x16{};
 
-    const int off0 = frag_offset(lane, 0), off1 = frag_offset(lane, 1);
-
-    auto compute = [&](const char *base) {
-        const char *At = base + (wm * 32 * RB) * 64;
-        const char *Bt = base + NC * A_BYTES + (wn * 64) * 64;
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-            const int off = s ? off1 : off0;
-            bf16x8 bfr[NC][2];
-#pragma unroll
-            for (int c = 0; c < NC; ++c)
-#pragma unroll
-                for (int cb = 0; cb < 2; ++cb)
-                    bfr[c][cb] = lds_frag(Bt + c * B_BYTES + cb * 32 * 64, off);
-            bf16x8 afr[RB];
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb) afr[rb] = lds_frag(At + rb * 32 * 64, off);
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-                for (int cb = 0; cb < 2; ++cb) hi[rb][cb] = mfma(afr[rb], bfr[0][cb], hi[rb][cb]);
-#pragma unroll
-            for (int j = 1; j < 3; ++j)
-#pragma unroll
-                for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-                    for (int cb = 0; cb < 2; ++cb) lo[rb][cb] = mfma(afr[rb], bfr[j][cb], lo[rb][cb]);
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb) afr[rb] = lds_frag(At + A_BYTES + rb * 32 * 64, off);
-#pragma unroll
-            for (int j = 0; j < 2; ++j)
-#pragma unroll
-                for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-                    for (int cb = 0; cb < 2; ++cb) lo[rb][cb] = mfma(afr[rb], bfr[j][cb], lo[rb][cb]);
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb) afr[rb] = lds_frag(At + 2 * A_BYTES + rb * 32 * 64, off);
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-                for (int cb = 0; cb < 2; ++cb) lo[rb][cb] = mfma(afr[rb], bfr[0][cb], lo[rb][cb]);
-        }
-    };
-
-    auto flush = [&]() {
+    // Outer loop: reduction panels of 256 (the FP32 reconstruction unit).
+    // Inner loop: k-blocks of 32, double-buffered; at the top of trip kb the copy
+    // of k-block kb has landed (own copies: vmcnt; other waves': barrier) and
+    // every wave has finished reading the other stage, which the copy of
+    // k-block kb + 1 then refills.
+    issue(0, stage0);
+    int kb = 0;
+    for (int p0 = 0; p0 < KB; p0 += KB_PER_PANEL) {
+        const int p1 = min(KB, p0 + KB_PER_PANEL);
+        f32x16 hi[RB][2], lo[RB][2];
 #pragma unroll
         for (int i = 0; i < RB; ++i)
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
-                blk[i][j] += lo[i][j] + hi[i][j];
                 hi[i][j] = f32x16{};
                 lo[i][j] = f32x16{};
             }
-    };
-
-    // Main loop.  At the top of trip kb the copy of k-block kb has landed
-    // (own copies: vmcnt; other waves': barrier) and every wave has finished
-    // reading the other stage, which the copy of k-block kb + 1 then refills.
-    issue(0, stage0);
-    for (int kb = 0; kb < KB; ++kb) {
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();
-        char *cur = (kb & 1) ? stage1 : stage0;
-        char *nxt = (kb & 1) ? stage0 : stage1;
-        if (kb + 1 < KB) issue(kb + 1, nxt);
-        compute(cur);
-        if (((kb + 1) % KB_PER_PANEL) == 0 || kb + 1 == KB) flush();
+        for (; kb < p1; ++kb) {
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __syncthreads();
+            char *cur = (kb & 1) ? stage1 : stage0;
+            char *nxt = (kb & 1) ? stage0 : stage1;
+            if (kb + 1 < KB) issue(kb + 1, nxt);
+            substep(cur, off0, hi, lo);
+            substep(cur, off1, hi, lo);
+        }
+#pragma unroll
+        for (int i = 0; i < RB; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) blk[i][j] += lo[i][j] + hi[i][j];
     }
 
     // Store the wave tile.

@@ -72,67 +72,64 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
         }
     };
 
-    f32x16 acc[K::P][BM];
+    const int off0 = frag_offset(lane, 0), off1 = frag_offset(lane, 1);
+
+    // One 16-index sub-step on the stage at `base`: every retained product.
+    auto substep = [&](const char *base, int off, f32x16 (&acc)[K::P][BM]) {
+        const char *At = base + (wm * 32 * BM) * 64;
+        const char *Bt = base + D * K::A_BYTES + (wn * 32) * 64;
+        bf16x8 af[D][BM], bf[D];
+#pragma unroll
+        for (int c = 0; c < D; ++c) {
+            bf[c] = lds_frag(Bt + c * K::B_BYTES, off);
+#pragma unroll
+            for (int b = 0; b < BM; ++b) af[c][b] = lds_frag(At + c * K::A_BYTES + b * 32 * 64, off);
+        }
+        // product q = l (l + 1) / 2 + i is A_i B_(l - i): diagonal l ascending,
+        // i ascending (all indices are compile-time constants after unrolling)
+#pragma unroll
+        for (int l = 0; l < D; ++l)
+#pragma unroll
+            for (int i = 0; i <= l; ++i)
+#pragma unroll
+                for (int b = 0; b < BM; ++b)
+                    acc[l * (l + 1) / 2 + i][b] =
+                        mfma(af[i][b], bf[l - i], acc[l * (l + 1) / 2 + i][b]);
+    };
+
     double acc64[BM][16];
-#pragma unroll
-    for (int q = 0; q < K::P; ++q)
-#pragma unroll
-        for (int b = 0; b < BM; ++b) acc[q][b] = f32x16{};
 #pragma unroll
     for (int b = 0; b < BM; ++b)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc64[b][r] = 0.0;
 
-    const int off0 = frag_offset(lane, 0), off1 = frag_offset(lane, 1);
-
-    auto compute = [&](const char *base) {
-        const char *At = base + (wm * 32 * BM) * 64;
-        const char *Bt = base + D * K::A_BYTES + (wn * 32) * 64;
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-            const int off = s ? off1 : off0;
-            bf16x8 af[D][BM], bf[D];
-#pragma unroll
-            for (int c = 0; c < D; ++c) {
-                bf[c] = lds_frag(Bt + c * K::B_BYTES, off);
-#pragma unroll
-                for (int b = 0; b < BM; ++b) af[c][b] = lds_frag(At + c * K::A_BYTES + b * 32 * 64, off);
-            }
-            // product q = l (l + 1) / 2 + i is A_i B_(l - i): diagonal l ascending,
-            // i ascending (all indices are compile-time constants after unrolling)
-#pragma unroll
-            for (int l = 0; l < D; ++l)
-#pragma unroll
-                for (int i = 0; i <= l; ++i)
-#pragma unroll
-                    for (int b = 0; b < BM; ++b)
-                        acc[l * (l + 1) / 2 + i][b] =
-                            mfma(af[i][b], bf[l - i], acc[l * (l + 1) / 2 + i][b]);
-        }
-    };
-
-    // Panel end: widen each product exactly and add it in FP64, in order.
-    auto epilogue = [&]() {
+    // Outer loop: reduction panels of 256; inner loop: double-buffered k-blocks
+    // (same schedule as the FP32 kernel).  After each panel every product is
+    // widened exactly and added in FP64, in the executed order.
+    issue(0, stage0);
+    int kb = 0;
+    for (int p0 = 0; p0 < KB; p0 += KB_PER_PANEL) {
+        const int p1 = min(KB, p0 + KB_PER_PANEL);
+        f32x16 acc[K::P][BM];
 #pragma unroll
         for (int q = 0; q < K::P; ++q)
 #pragma unroll
-            for (int b = 0; b < BM; ++b) {
+            for (int b = 0; b < BM; ++b) acc[q][b] = f32x16{};
+        for (; kb < p1; ++kb) {
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __syncthreads();
+            char *cur = (kb & 1) ? stage1 : stage0;
+            char *nxt = (kb & 1) ? stage0 : stage1;
+            if (kb + 1 < KB) issue(kb + 1, nxt);
+            substep(cur, off0, acc);
+            substep(cur, off1, acc);
+        }
+#pragma unroll
+        for (int q = 0; q < K::P; ++q)
+#pragma unroll
+            for (int b = 0; b < BM; ++b)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc64[b][r] += (double)acc[q][b][r];
-                acc[q][b] = f32x16{};
-            }
-    };
-
-    // Main loop: same double-buffered schedule as the FP32 kernel.
-    issue(0, stage0);
-    for (int kb = 0; kb < KB; ++kb) {
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();
-        char *cur = (kb & 1) ? stage1 : stage0;
-        char *nxt = (kb & 1) ? stage0 : stage1;
-        if (kb + 1 < KB) issue(kb + 1, nxt);
-        compute(cur);
-        if (((kb + 1) % KB_PER_PANEL) == 0 || kb + 1 == KB) epilogue();
     }
 
 #pragma unroll
