@@ -75,7 +75,9 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
     const int off0 = frag_offset(lane, 0), off1 = frag_offset(lane, 1);
 
     // One 16-index sub-step on the stage at `base`: every retained product.
-    auto substep = [&](const char *base, int off, f32x16 (&acc)[K::P][BM]) {
+    // first: the panel's first sub-step, whose MFMAs start from zero (no
+    // separate zeroing of the accumulators, so no second live set).
+    auto substep = [&](const char *base, int off, f32x16 (&acc)[K::P][BM], bool first) {
         const char *At = base + (wm * 32 * BM) * 64;
         const char *Bt = base + D * K::A_BYTES + (wn * 32) * 64;
         bf16x8 af[D][BM], bf[D];
@@ -94,7 +96,7 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
 #pragma unroll
                 for (int b = 0; b < BM; ++b)
                     acc[l * (l + 1) / 2 + i][b] =
-                        mfma(af[i][b], bf[l - i], acc[l * (l + 1) / 2 + i][b]);
+                        mfma(af[i][b], bf[l - i], first ? f32x16{} : acc[l * (l + 1) / 2 + i][b]);
     };
 
     double acc64[BM][16];
@@ -111,18 +113,24 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
     for (int p0 = 0; p0 < KB; p0 += KB_PER_PANEL) {
         const int p1 = min(KB, p0 + KB_PER_PANEL);
         f32x16 acc[K::P][BM];
-#pragma unroll
-        for (int q = 0; q < K::P; ++q)
-#pragma unroll
-            for (int b = 0; b < BM; ++b) acc[q][b] = f32x16{};
+        {   // first k-block of the panel (peeled: its first sub-step starts from zero)
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __syncthreads();
+            char *cur = (kb & 1) ? stage1 : stage0;
+            char *nxt = (kb & 1) ? stage0 : stage1;
+            if (kb + 1 < KB) issue(kb + 1, nxt);
+            substep(cur, off0, acc, true);
+            substep(cur, off1, acc, false);
+            ++kb;
+        }
         for (; kb < p1; ++kb) {
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
             __syncthreads();
             char *cur = (kb & 1) ? stage1 : stage0;
             char *nxt = (kb & 1) ? stage0 : stage1;
             if (kb + 1 < KB) issue(kb + 1, nxt);
-            substep(cur, off0, acc);
-            substep(cur, off1, acc);
+            substep(cur, off0, acc, false);
+            substep(cur, off1, acc, false);
         }
 #pragma unroll
         for (int q = 0; q < K::P; ++q)
