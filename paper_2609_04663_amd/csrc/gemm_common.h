@@ -39,7 +39,7 @@ __device__ inline void copy_1k(const char *src_wave, char *lds_dst, int lane) {
 __device__ inline int frag_offset(int lane, int s) {
     const int row = lane & 31;
     const int q = 2 * s + (lane >> 5);
-    return row * 64 + ((q ^ ((row >> 1) & 3)) << 4);
+    return row * 64 + ((q ^ swz(row)) << 4);
 }
 
 __device__ inline bf16x8 lds_frag(const char *tile_block, int off) {
@@ -48,6 +48,35 @@ __device__ inline bf16x8 lds_frag(const char *tile_block, int off) {
 
 __device__ inline f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// MFMA whose accumulator is pinned to VGPRs (the builtin's accumulators live
+// in AGPRs; a kernel with more than 256 accumulator registers would otherwise
+// have them shuffled between the two files every iteration).  The compiler
+// does not see inside the asm, so a VALU read of the result must go through
+// mfma_vacc_settle first (wait states for the MFMA write, see below).
+__device__ inline void mfma_vacc(f32x16 &c, bf16x8 a, bf16x8 b) {
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(c) : "v"(a), "v"(b));
+}
+__device__ inline void mfma_vacc_zero(f32x16 &c, bf16x8 a, bf16x8 b) {
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=v"(c) : "v"(a), "v"(b));
+}
+// Wait states before VALU instructions may read an inline-asm MFMA result
+// (the hardware does not interlock this; 24 is above what a 32x32x16 MFMA
+// needs).  Taking c as an operand orders every later reader after it.
+__device__ inline void mfma_vacc_settle(f32x16 &c) {
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(c));
+}
+
+// Workgroup barrier for the k-loop pipeline.  The caller has already issued
+// the s_waitcnt it needs (its own LDS reads done, its copies of the next stage
+// landed); unlike __syncthreads() this does not also wait for the copies that
+// are still meant to be in flight.  The empty asm statements keep the compiler
+// from moving memory accesses across the barrier.
+__device__ inline void pipeline_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
 }
 
 // Output coordinates of accumulator register r of lane l in a 32x32 block:

@@ -48,62 +48,75 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
     const int64_t a_plane = (int64_t)KB * RpadA * 64;
     const int64_t b_plane = (int64_t)KB * RpadB * 64;
 
-    // Copy issue: a runtime loop keeps the per-chunk addresses out of registers.
+    // Copy issue for one k-block: wave w moves 1 KB parts [3w, 3w + 3) of each A
+    // plane and [2w, 2w + 2) of each B plane, so every address is a wave-uniform
+    // base plus a compile-time offset.
+    static_assert(A_BYTES / 1024 == 12 && B_BYTES / 1024 == 8, "part split assumes 192 x 128");
+    const int64_t a_base = m0 * 64 + wave * 3 * 1024;
+    const int64_t b_base = n0 * 64 + wave * 2 * 1024;
     auto issue = [&](int kb, char *base) {
-#pragma unroll 1
-        for (int i = 0; i < A_CHUNKS / 4; ++i) {
-            const int ch = wave * (A_CHUNKS / 4) + i;
-            const int c = ch / (A_BYTES / 1024), part = ch % (A_BYTES / 1024);
-            const char *src = Ag + c * a_plane + ((int64_t)kb * RpadA + m0) * 64 + part * 1024;
-            copy_1k(src, base + c * A_BYTES + part * 1024, lane);
-        }
-#pragma unroll 1
-        for (int i = 0; i < B_CHUNKS / 4; ++i) {
-            const int ch = wave * (B_CHUNKS / 4) + i;
-            const int c = ch / (B_BYTES / 1024), part = ch % (B_BYTES / 1024);
-            const char *src = Bg + c * b_plane + ((int64_t)kb * RpadB + n0) * 64 + part * 1024;
-            copy_1k(src, base + NC * A_BYTES + c * B_BYTES + part * 1024, lane);
-        }
+        const char *a_src = Ag + (int64_t)kb * RpadA * 64 + a_base;
+        const char *b_src = Bg + (int64_t)kb * RpadB * 64 + b_base;
+        char *a_dst = base + wave * 3 * 1024;
+        char *b_dst = base + NC * A_BYTES + wave * 2 * 1024;
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int j = 0; j < 3; ++j)
+                copy_1k(a_src + c * a_plane + j * 1024, a_dst + c * A_BYTES + j * 1024, lane);
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                copy_1k(b_src + c * b_plane + j * 1024, b_dst + c * B_BYTES + j * 1024, lane);
     };
 
     const int off0 = frag_offset(lane, 0), off1 = frag_offset(lane, 1);
 
-    // One 16-index sub-step on the stage at `base`: 36 MFMAs into hi / lo.
-    auto substep = [&](const char *base, int off, f32x16 (&hi)[RB][2], f32x16 (&lo)[RB][2]) {
+    // Fragments of one 16-index sub-step: the three B planes (2 column blocks)
+    // and the three A planes (RB row blocks).
+    struct Frags {
+        bf16x8 b[NC][2];
+        bf16x8 a[NC][RB];
+    };
+    auto load = [&](const char *base, int off, Frags &f) {
         const char *At = base + (wm * 32 * RB) * 64;
         const char *Bt = base + NC * A_BYTES + (wn * 64) * 64;
-        bf16x8 bfr[NC][2];
 #pragma unroll
-        for (int c = 0; c < NC; ++c)
+        for (int c = 0; c < NC; ++c) {
 #pragma unroll
-            for (int cb = 0; cb < 2; ++cb) bfr[c][cb] = lds_frag(Bt + c * B_BYTES + cb * 32 * 64, off);
-        bf16x8 afr[RB];
+            for (int cb = 0; cb < 2; ++cb) f.b[c][cb] = lds_frag(Bt + c * B_BYTES + cb * 32 * 64, off);
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) afr[rb] = lds_frag(At + rb * 32 * 64, off);
+            for (int rb = 0; rb < RB; ++rb) f.a[c][rb] = lds_frag(At + c * A_BYTES + rb * 32 * 64, off);
+        }
+    };
+    // The six products on one sub-step: A0B0 into hi, A0B1 A0B2 A1B0 A1B1 A2B0
+    // into lo.  zero: the panel's first sub-step (accumulators start at 0).
+    auto mma = [&](const Frags &f, f32x16 (&hi)[RB][2], f32x16 (&lo)[RB][2], bool zero) {
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-            for (int cb = 0; cb < 2; ++cb) hi[rb][cb] = mfma(afr[rb], bfr[0][cb], hi[rb][cb]);
+            for (int cb = 0; cb < 2; ++cb)
+                hi[rb][cb] = mfma(f.a[0][rb], f.b[0][cb], zero ? f32x16{} : hi[rb][cb]);
 #pragma unroll
-        for (int j = 1; j < 3; ++j)
+        for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
+            for (int cb = 0; cb < 2; ++cb)
+                lo[rb][cb] = mfma(f.a[0][rb], f.b[1][cb], zero ? f32x16{} : lo[rb][cb]);
 #pragma unroll
-                for (int cb = 0; cb < 2; ++cb) lo[rb][cb] = mfma(afr[rb], bfr[j][cb], lo[rb][cb]);
+        for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) afr[rb] = lds_frag(At + A_BYTES + rb * 32 * 64, off);
+            for (int cb = 0; cb < 2; ++cb) lo[rb][cb] = mfma(f.a[0][rb], f.b[2][cb], lo[rb][cb]);
 #pragma unroll
         for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-                for (int cb = 0; cb < 2; ++cb) lo[rb][cb] = mfma(afr[rb], bfr[j][cb], lo[rb][cb]);
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) afr[rb] = lds_frag(At + 2 * A_BYTES + rb * 32 * 64, off);
+                for (int cb = 0; cb < 2; ++cb) lo[rb][cb] = mfma(f.a[1][rb], f.b[j][cb], lo[rb][cb]);
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-            for (int cb = 0; cb < 2; ++cb) lo[rb][cb] = mfma(afr[rb], bfr[0][cb], lo[rb][cb]);
+            for (int cb = 0; cb < 2; ++cb) lo[rb][cb] = mfma(f.a[2][rb], f.b[0][cb], lo[rb][cb]);
     };
 
     f32x16 blk[RB][2];
@@ -112,37 +125,62 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
 #pragma unroll
         for (int j = 0; j < 2; ++j) blk[i][j] = f32x16{};
 
-    // Outer loop: reduction panels of 256 (the FP32 reconstruction unit).
-    // Inner loop: k-blocks of 32, double-buffered; at the top of trip kb the copy
-    // of k-block kb has landed (own copies: vmcnt; other waves': barrier) and
-    // every wave has finished reading the other stage, which the copy of
-    // k-block kb + 1 then refills.
+    // Software pipeline over k-blocks (two LDS stages).  Entering trip kb the
+    // sub-step-0 fragments of kb are in registers and the copy of kb + 1 is in
+    // flight.  The trip (1) reads the sub-step-1 fragments of kb while the
+    // sub-step-0 MFMAs run; (2) waits for its own copies of kb + 1 and its LDS
+    // reads, then barriers: now every wave is done reading stage kb and every
+    // copy of kb + 1 has landed; (3) starts the copy of kb + 2 into stage kb and
+    // reads the sub-step-0 fragments of kb + 1 while the sub-step-1 MFMAs run.
     issue(0, stage0);
+    if (KB > 1) issue(1, stage1);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    Frags f0, f1;
+    load(stage0, off0, f0);
     int kb = 0;
     for (int p0 = 0; p0 < KB; p0 += KB_PER_PANEL) {
         const int p1 = min(KB, p0 + KB_PER_PANEL);
         f32x16 hi[RB][2], lo[RB][2];
-#pragma unroll
-        for (int i = 0; i < RB; ++i)
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                hi[i][j] = f32x16{};
-                lo[i][j] = f32x16{};
-            }
-        for (; kb < p1; ++kb) {
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-            __syncthreads();
+        auto kblock = [&](bool first) {
             char *cur = (kb & 1) ? stage1 : stage0;
             char *nxt = (kb & 1) ? stage0 : stage1;
-            if (kb + 1 < KB) issue(kb + 1, nxt);
-            substep(cur, off0, hi, lo);
-            substep(cur, off1, hi, lo);
-        }
+            load(cur, off1, f1);
+            mma(f0, hi, lo, first);
+            // 15 fragment reads spread over the 36 MFMAs of sub-step 0
+#pragma unroll
+            for (int i = 0; i < 15; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+                __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // MFMA
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+            pipeline_barrier();
+            // the copy past the last k-block re-reads the last one (in bounds, unused)
+            issue(min(kb + 2, KB - 1), cur);
+            load(nxt, off0, f0);      // unused after the last k-block; always in bounds
+            mma(f1, hi, lo, false);
+            // 15 copies and 15 fragment reads spread over the 36 MFMAs of sub-step 1
+#pragma unroll
+            for (int i = 0; i < 15; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 1);   // VMEM read (copy)
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);   // DS read
+                __builtin_amdgcn_sched_group_barrier(0x008, 2, 1);   // MFMA
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, 6, 1);
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        kblock(true);                 // panel's first k-block: accumulators start at 0
+        for (++kb; kb < p1; ++kb) kblock(false);
 #pragma unroll
         for (int i = 0; i < RB; ++i)
 #pragma unroll
             for (int j = 0; j < 2; ++j) blk[i][j] += lo[i][j] + hi[i][j];
     }
+    // the last trips issued (unused) copies: let them land before the workgroup
+    // ends and its LDS is handed to another workgroup
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
     // Store the wave tile.
 #pragma unroll

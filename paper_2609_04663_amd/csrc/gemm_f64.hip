@@ -14,34 +14,45 @@
 //
 // Workgroup: 4 waves in a 2 x 2 grid; wave tile (32 BM) x 32, output tile
 // (64 BM) x 64.  Per k-block of 32 the d planes of both operands are copied
-// straight into LDS (global_load_lds_dwordx4), double-buffered.  Each wave
-// keeps one FP32 accumulator set per product for the whole panel (all N_p
-// live, so every fragment read from LDS feeds every product that uses it) and
-// an FP64 accumulator tile.
+// straight into LDS (global_load_lds_dwordx4) through a ring of LDS stages.
+// Each wave keeps one FP32 accumulator set per product for the whole panel
+// (all N_p live, so every fragment read from LDS feeds every product that
+// uses it) and an FP64 accumulator tile.
 #include "gemm_common.h"
 
 namespace emu {
 namespace {
 
-template <int D, int BM>
+template <int D, int BM, int NS, bool ACC64_LDS>
 struct Cfg {
-    static constexpr int P = D * (D + 1) / 2;
+    static constexpr int P = D * (D + 1) / 2;       // retained products N_p(d)
+    // FP64 accumulator tile in LDS instead of registers (frees 32 BM VGPRs for
+    // the N_p FP32 accumulator sets; touched once per panel)
+    static constexpr int ACC64_BYTES = ACC64_LDS ? 4 * 64 * 16 * BM * 8 : 0;
+    // products q >= Q_VGPR keep their accumulators in VGPRs (inline-asm MFMA)
+    // so that all N_p sets fit: 256 AGPRs hold 16 sets of 16 registers
+    static constexpr int Q_VGPR = P * BM > 16 ? 16 / BM : P;
     static constexpr int MT = 64 * BM, NT = DGEMM_NT;
     static constexpr int A_BYTES = MT * 64, B_BYTES = NT * 64;
     static constexpr int STAGE = D * (A_BYTES + B_BYTES);
+    static constexpr int NSTAGE = NS;               // LDS stages (copy lead = NS - 1 k-blocks)
     static constexpr int A_PARTS = A_BYTES / 1024, B_PARTS = B_BYTES / 1024;
-    static constexpr int CHUNKS = D * (A_PARTS + B_PARTS);
-    static_assert(CHUNKS % 4 == 0, "chunks must split evenly over 4 waves");
-    static_assert(2 * STAGE <= 160 * 1024, "LDS");
+    static constexpr int COPIES = D * (A_PARTS + B_PARTS) / 4;   // 1 KB copies per wave per k-block
+    static constexpr int READS = D * (BM + 1);      // fragment reads per sub-step
+    static constexpr int MMAS = P * BM;             // MFMAs per sub-step
+    static_assert(A_PARTS == 4 * BM && B_PARTS == 4, "copy split assumes 4 waves");
+    static_assert(NS * STAGE + ACC64_BYTES <= 160 * 1024, "LDS");
 };
 
-template <int D, int BM>
+template <int D, int BM, int NS, bool ACC64_LDS>
 __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
     const uint16_t *__restrict__ Ap, const uint16_t *__restrict__ Bp, double *__restrict__ C,
     int64_t M, int64_t N, int KB, int64_t RpadA, int64_t RpadB, int64_t ldc, int nt_m, int nt_n) {
-    using K = Cfg<D, BM>;
-    __shared__ __attribute__((aligned(1024))) char stage0[K::STAGE];
-    __shared__ __attribute__((aligned(1024))) char stage1[K::STAGE];
+    using K = Cfg<D, BM, NS, ACC64_LDS>;
+    __shared__ __attribute__((aligned(1024))) char lds[K::NSTAGE * K::STAGE + K::ACC64_BYTES];
+    // lane-private FP64 accumulators in LDS: element r of lane l of wave w at
+    // ((w * BM + b) * 16 + r) * 64 + l (consecutive lanes, consecutive doubles)
+    double *acc64_lds = reinterpret_cast<double *>(lds + K::NSTAGE * K::STAGE);
 
     int tm, tn;
     tile_coords<8>(nt_m, nt_n, tm, tn);
@@ -55,90 +66,153 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
     const int64_t a_plane = (int64_t)KB * RpadA * 64;
     const int64_t b_plane = (int64_t)KB * RpadB * 64;
 
+    // Copy issue for one k-block: wave w moves 1 KB parts [w BM, (w + 1) BM) of
+    // every A plane and part w of every B plane (wave-uniform base plus
+    // compile-time offsets).
+    const int64_t a_base = m0 * 64 + (int64_t)wave * BM * 1024;
+    const int64_t b_base = n0 * 64 + (int64_t)wave * 1024;
     auto issue = [&](int kb, char *base) {
-#pragma unroll 1
-        for (int i = 0; i < K::CHUNKS / 4; ++i) {
-            const int ch = wave + 4 * i;
-            if (ch < D * K::A_PARTS) {
-                const int c = ch / K::A_PARTS, part = ch % K::A_PARTS;
-                const char *src = Ag + c * a_plane + ((int64_t)kb * RpadA + m0) * 64 + part * 1024;
-                copy_1k(src, base + c * K::A_BYTES + part * 1024, lane);
-            } else {
-                const int cc = ch - D * K::A_PARTS;
-                const int c = cc / K::B_PARTS, part = cc % K::B_PARTS;
-                const char *src = Bg + c * b_plane + ((int64_t)kb * RpadB + n0) * 64 + part * 1024;
-                copy_1k(src, base + D * K::A_BYTES + c * K::B_BYTES + part * 1024, lane);
-            }
+        const char *a_src = Ag + (int64_t)kb * RpadA * 64 + a_base;
+        const char *b_src = Bg + (int64_t)kb * RpadB * 64 + b_base;
+        char *a_dst = base + wave * BM * 1024;
+        char *b_dst = base + D * K::A_BYTES + wave * 1024;
+#pragma unroll
+        for (int c = 0; c < D; ++c) {
+#pragma unroll
+            for (int j = 0; j < BM; ++j)
+                copy_1k(a_src + c * a_plane + j * 1024, a_dst + c * K::A_BYTES + j * 1024, lane);
+            copy_1k(b_src + c * b_plane, b_dst + c * K::B_BYTES, lane);
         }
     };
+    auto stage = [&](int kb) -> char * { return lds + (kb % K::NSTAGE) * K::STAGE; };
 
     const int off0 = frag_offset(lane, 0), off1 = frag_offset(lane, 1);
 
-    // One 16-index sub-step on the stage at `base`: every retained product.
-    // first: the panel's first sub-step, whose MFMAs start from zero (no
-    // separate zeroing of the accumulators, so no second live set).
-    auto substep = [&](const char *base, int off, f32x16 (&acc)[K::P][BM], bool first) {
+    // Fragments of one 16-index sub-step: D planes of A (BM row blocks) and of B.
+    struct Frags {
+        bf16x8 a[D][BM], b[D];
+    };
+    // Slice m (A_m and B_m) of a sub-step.
+    auto load_slice = [&](const char *base, int off, Frags &f, int m) {
         const char *At = base + (wm * 32 * BM) * 64;
         const char *Bt = base + D * K::A_BYTES + (wn * 32) * 64;
-        bf16x8 af[D][BM], bf[D];
+        f.b[m] = lds_frag(Bt + m * K::B_BYTES, off);
 #pragma unroll
-        for (int c = 0; c < D; ++c) {
-            bf[c] = lds_frag(Bt + c * K::B_BYTES, off);
+        for (int b = 0; b < BM; ++b) f.a[m][b] = lds_frag(At + m * K::A_BYTES + b * 32 * 64, off);
+    };
+    auto load = [&](const char *base, int off, Frags &f) {
 #pragma unroll
-            for (int b = 0; b < BM; ++b) af[c][b] = lds_frag(At + c * K::A_BYTES + b * 32 * 64, off);
+        for (int m = D - 1; m >= 0; --m) load_slice(base, off, f, m);
+    };
+    // The products with max(i, j) = m (i + j < D).  Product q = l (l + 1) / 2 + i
+    // is A_i B_(l - i): its accumulator index encodes the FP64 order (diagonal l
+    // ascending, i ascending), which the panel-end epilogue follows; the MFMA
+    // issue order inside a panel does not matter (exact panel sums).
+    auto mma_group = [&](const Frags &f, f32x16 (&acc)[K::P][BM], int m, bool zero) {
+#pragma unroll
+        for (int i = 0; i <= m; ++i)
+#pragma unroll
+            for (int j = 0; j <= m; ++j) {
+                if ((i != m && j != m) || i + j >= D) continue;
+                const int q = (i + j) * (i + j + 1) / 2 + i;
+#pragma unroll
+                for (int b = 0; b < BM; ++b) {
+                    if (q >= K::Q_VGPR) {
+                        if (zero) mfma_vacc_zero(acc[q][b], f.a[i][b], f.b[j]);
+                        else mfma_vacc(acc[q][b], f.a[i][b], f.b[j]);
+                    } else {
+                        acc[q][b] = mfma(f.a[i][b], f.b[j], zero ? f32x16{} : acc[q][b]);
+                    }
+                }
+            }
+    };
+    // One sub-step on `cur` while the same slices of the next sub-step are read
+    // from `nbase`: group m (the last use of slice m) is followed by the read of
+    // slice m of the next sub-step into the registers it frees.  Groups run from
+    // m = D - 1 down to 0, the order in which the next sub-step needs them.
+    auto step = [&](const Frags &cur, f32x16 (&acc)[K::P][BM], bool zero, const char *nbase,
+                    int noff, Frags &nxt) {
+#pragma unroll
+        for (int m = D - 1; m >= 0; --m) {
+            mma_group(cur, acc, m, zero);
+            load_slice(nbase, noff, nxt, m);
         }
-        // product q = l (l + 1) / 2 + i is A_i B_(l - i): diagonal l ascending,
-        // i ascending (all indices are compile-time constants after unrolling)
-#pragma unroll
-        for (int l = 0; l < D; ++l)
-#pragma unroll
-            for (int i = 0; i <= l; ++i)
-#pragma unroll
-                for (int b = 0; b < BM; ++b)
-                    acc[l * (l + 1) / 2 + i][b] =
-                        mfma(af[i][b], bf[l - i], first ? f32x16{} : acc[l * (l + 1) / 2 + i][b]);
     };
 
-    double acc64[BM][16];
+    double acc64[ACC64_LDS ? 1 : BM][16];
 #pragma unroll
     for (int b = 0; b < BM; ++b)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc64[b][r] = 0.0;
+        for (int r = 0; r < 16; ++r) {
+            if constexpr (ACC64_LDS)
+                acc64_lds[((wave * BM + b) * 16 + r) * 64 + lane] = 0.0;
+            else
+                acc64[b][r] = 0.0;
+        }
 
-    // Outer loop: reduction panels of 256; inner loop: double-buffered k-blocks
-    // (same schedule as the FP32 kernel).  After each panel every product is
-    // widened exactly and added in FP64, in the executed order.
-    issue(0, stage0);
+    // Software pipeline over k-blocks with a ring of NS LDS stages (stage of
+    // k-block kb: kb mod NS).  Entering trip kb the sub-step-0 fragments of kb
+    // are in registers and the copies of kb + 1 .. kb + NS - 1 have been
+    // issued.  The trip (1) reads the sub-step-1 fragments of kb while the
+    // sub-step-0 MFMAs run; (2) waits until at most the newest NS - 2 batches of
+    // its own copies are outstanding (so kb + 1 has landed) and for its LDS
+    // reads, then barriers: every wave is done reading stage kb and every copy
+    // of kb + 1 has landed; (3) starts the copy of kb + NS into stage kb and
+    // reads the sub-step-0 fragments of kb + 1 while the sub-step-1 MFMAs run.
+    // Copies past the last k-block re-read the last one (in bounds, unused).
+    for (int j = 0; j < K::NSTAGE; ++j) issue(min(j, KB - 1), stage(j));
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((K::NSTAGE - 1) * K::COPIES) : "memory");
+    __syncthreads();
+    Frags f0, f1;
+    load(stage(0), off0, f0);
     int kb = 0;
     for (int p0 = 0; p0 < KB; p0 += KB_PER_PANEL) {
         const int p1 = min(KB, p0 + KB_PER_PANEL);
         f32x16 acc[K::P][BM];
-        {   // first k-block of the panel (peeled: its first sub-step starts from zero)
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-            __syncthreads();
-            char *cur = (kb & 1) ? stage1 : stage0;
-            char *nxt = (kb & 1) ? stage0 : stage1;
-            if (kb + 1 < KB) issue(kb + 1, nxt);
-            substep(cur, off0, acc, true);
-            substep(cur, off1, acc, false);
-            ++kb;
-        }
-        for (; kb < p1; ++kb) {
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-            __syncthreads();
-            char *cur = (kb & 1) ? stage1 : stage0;
-            char *nxt = (kb & 1) ? stage0 : stage1;
-            if (kb + 1 < KB) issue(kb + 1, nxt);
-            substep(cur, off0, acc, false);
-            substep(cur, off1, acc, false);
-        }
+        auto kblock = [&](bool first) {
+            char *cur = stage(kb);
+            step(f0, acc, first, cur, off1, f1);          // sub-step 0; reads sub-step 1
+            __builtin_amdgcn_sched_barrier(0);
+            if constexpr (K::NSTAGE == 2)
+                asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+            else
+                asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"((K::NSTAGE - 2) * K::COPIES)
+                             : "memory");
+            pipeline_barrier();
+            issue(min(kb + K::NSTAGE, KB - 1), cur);
+            step(f1, acc, false, stage(kb + 1), off0, f0); // sub-step 1; reads next sub-step 0
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        kblock(true);
+        for (++kb; kb < p1; ++kb) kblock(false);
+        // panel end: widen each product exactly and add it in FP64, in order
 #pragma unroll
-        for (int q = 0; q < K::P; ++q)
+        for (int q = K::Q_VGPR; q < K::P; ++q)
+#pragma unroll
+            for (int b = 0; b < BM; ++b) mfma_vacc_settle(acc[q][b]);
+        if constexpr (ACC64_LDS) {
 #pragma unroll
             for (int b = 0; b < BM; ++b)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) acc64[b][r] += (double)acc[q][b][r];
+                for (int r = 0; r < 16; ++r) {
+                    double *slot = &acc64_lds[((wave * BM + b) * 16 + r) * 64 + lane];
+                    double t = *slot;
+#pragma unroll
+                    for (int q = 0; q < K::P; ++q) t += (double)acc[q][b][r];
+                    *slot = t;
+                }
+        } else {
+#pragma unroll
+            for (int q = 0; q < K::P; ++q)
+#pragma unroll
+                for (int b = 0; b < BM; ++b)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) acc64[b][r] += (double)acc[q][b][r];
+        }
     }
+    // the last trips issued (unused) copies: let them land before the workgroup
+    // ends and its LDS is handed to another workgroup
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
 #pragma unroll
     for (int b = 0; b < BM; ++b) {
@@ -146,17 +220,19 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int64_t row = m0 + wm * 32 * BM + b * 32 + acc_row(lane, r);
-            if (row < M && col < N) C[row * ldc + col] = acc64[b][r];
+            if (row < M && col < N)
+                C[row * ldc + col] = ACC64_LDS ? acc64_lds[((wave * BM + b) * 16 + r) * 64 + lane]
+                                               : acc64[ACC64_LDS ? 0 : b][r];
         }
     }
 }
 
-template <int D, int BM>
+template <int D, int BM, int NS, bool ACC64_LDS>
 hipError_t launch_t(const uint16_t *Ap, const uint16_t *Bp, double *C, int64_t M, int64_t N,
                     int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc, hipStream_t s) {
-    using K = Cfg<D, BM>;
+    using K = Cfg<D, BM, NS, ACC64_LDS>;
     const int nt_m = (int)((M + K::MT - 1) / K::MT), nt_n = (int)((N + K::NT - 1) / K::NT);
-    gemm_f64_kernel<D, BM><<<nt_m * nt_n, 256, 0, s>>>(Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc,
+    gemm_f64_kernel<D, BM, NS, ACC64_LDS><<<nt_m * nt_n, 256, 0, s>>>(Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc,
                                                        nt_m, nt_n);
     return hipGetLastError();
 }
@@ -167,10 +243,10 @@ hipError_t launch_gemm_f64(const uint16_t *Ap, const uint16_t *Bp, double *C, in
                            int64_t N, int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc,
                            int d, hipStream_t s) {
     switch (d) {
-        case 3: return launch_t<3, 2>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, s);
-        case 4: return launch_t<4, 1>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, s);
-        case 5: return launch_t<5, 1>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, s);
-        case 6: return launch_t<6, 1>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, s);
+        case 3: return launch_t<3, 2, 3, false>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, s);
+        case 4: return launch_t<4, 1, 3, false>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, s);
+        case 5: return launch_t<5, 1, 3, false>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, s);
+        case 6: return launch_t<6, 1, 2, true>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, s);
         default: return hipErrorInvalidValue;
     }
 }
