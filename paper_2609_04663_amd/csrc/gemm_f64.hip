@@ -71,19 +71,24 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
     // compile-time offsets).
     const int64_t a_base = m0 * 64 + (int64_t)wave * BM * 1024;
     const int64_t b_base = n0 * 64 + (int64_t)wave * 1024;
-    auto issue = [&](int kb, char *base) {
+    // Copies [j0, j1) of one k-block's COPIES: copy j moves plane c = j / (BM + 1),
+    // A part j % (BM + 1) (or the B part when that is BM).
+    auto issue = [&](int kb, char *base, int j0, int j1) {
         const char *a_src = Ag + (int64_t)kb * RpadA * 64 + a_base;
         const char *b_src = Bg + (int64_t)kb * RpadB * 64 + b_base;
         char *a_dst = base + wave * BM * 1024;
         char *b_dst = base + D * K::A_BYTES + wave * 1024;
 #pragma unroll
-        for (int c = 0; c < D; ++c) {
-#pragma unroll
-            for (int j = 0; j < BM; ++j)
-                copy_1k(a_src + c * a_plane + j * 1024, a_dst + c * K::A_BYTES + j * 1024, lane);
-            copy_1k(b_src + c * b_plane, b_dst + c * K::B_BYTES, lane);
+        for (int j = 0; j < K::COPIES; ++j) {
+            if (j < j0 || j >= j1) continue;
+            const int c = j / (BM + 1), r = j % (BM + 1);
+            if (r < BM)
+                copy_1k(a_src + c * a_plane + r * 1024, a_dst + c * K::A_BYTES + r * 1024, lane);
+            else
+                copy_1k(b_src + c * b_plane, b_dst + c * K::B_BYTES, lane);
         }
     };
+    constexpr int H0 = K::COPIES / 2;        // copies issued right after the barrier
     auto stage = [&](int kb) -> char * { return lds + (kb % K::NSTAGE) * K::STAGE; };
 
     const int off0 = frag_offset(lane, 0), off1 = frag_offset(lane, 1);
@@ -151,17 +156,21 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
         }
 
     // Software pipeline over k-blocks with a ring of NS LDS stages (stage of
-    // k-block kb: kb mod NS).  Entering trip kb the sub-step-0 fragments of kb
-    // are in registers and the copies of kb + 1 .. kb + NS - 1 have been
-    // issued.  The trip (1) reads the sub-step-1 fragments of kb while the
-    // sub-step-0 MFMAs run; (2) waits until at most the newest NS - 2 batches of
-    // its own copies are outstanding (so kb + 1 has landed) and for its LDS
-    // reads, then barriers: every wave is done reading stage kb and every copy
-    // of kb + 1 has landed; (3) starts the copy of kb + NS into stage kb and
-    // reads the sub-step-0 fragments of kb + 1 while the sub-step-1 MFMAs run.
-    // Copies past the last k-block re-read the last one (in bounds, unused).
-    for (int j = 0; j < K::NSTAGE; ++j) issue(min(j, KB - 1), stage(j));
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((K::NSTAGE - 1) * K::COPIES) : "memory");
+    // k-block kb: kb mod NS).  The copy of k-block kb + NS goes to stage kb,
+    // which is free once trip kb's barrier has passed: its first H0 copies are
+    // issued right after that barrier, the rest in trip kb + 1 before its
+    // barrier, so the copy instructions are spread over the whole k-block.
+    // Trip kb (1) issues the second half of k-block kb + NS - 1 and reads the
+    // sub-step-1 fragments of kb while the sub-step-0 MFMAs run; (2) waits until
+    // at most the newest NS - 2 k-blocks of its own copies are outstanding (so
+    // kb + 1 has landed) and for its LDS reads, then barriers: every wave is
+    // done reading stage kb and every copy of kb + 1 has landed; (3) issues the
+    // first half of k-block kb + NS into stage kb and reads the sub-step-0
+    // fragments of kb + 1 while the sub-step-1 MFMAs run.  Copies past the last
+    // k-block re-read the last one (in bounds, never used).
+    for (int j = 0; j < K::NSTAGE - 1; ++j) issue(min(j, KB - 1), stage(j), 0, K::COPIES);
+    issue(min(K::NSTAGE - 1, KB - 1), stage(K::NSTAGE - 1), 0, H0);
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((K::NSTAGE - 2) * K::COPIES + H0) : "memory");
     __syncthreads();
     Frags f0, f1;
     load(stage(0), off0, f0);
@@ -171,6 +180,7 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
         f32x16 acc[K::P][BM];
         auto kblock = [&](bool first) {
             char *cur = stage(kb);
+            issue(min(kb + K::NSTAGE - 1, KB - 1), stage(kb + K::NSTAGE - 1), H0, K::COPIES);
             step(f0, acc, first, cur, off1, f1);          // sub-step 0; reads sub-step 1
             __builtin_amdgcn_sched_barrier(0);
             if constexpr (K::NSTAGE == 2)
@@ -179,7 +189,7 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
                 asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"((K::NSTAGE - 2) * K::COPIES)
                              : "memory");
             pipeline_barrier();
-            issue(min(kb + K::NSTAGE, KB - 1), cur);
+            issue(min(kb + K::NSTAGE, KB - 1), cur, 0, H0);
             step(f1, acc, false, stage(kb + 1), off0, f0); // sub-step 1; reads next sub-step 0
             __builtin_amdgcn_sched_barrier(0);
         };
@@ -191,15 +201,24 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
 #pragma unroll
             for (int b = 0; b < BM; ++b) mfma_vacc_settle(acc[q][b]);
         if constexpr (ACC64_LDS) {
+            // eight elements at a time: eight independent FP64 chains keep the
+            // FP64 adder busy (one element's 21 adds in a row would wait on
+            // each other)
 #pragma unroll
             for (int b = 0; b < BM; ++b)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    double *slot = &acc64_lds[((wave * BM + b) * 16 + r) * 64 + lane];
-                    double t = *slot;
+                for (int h = 0; h < 16; h += 8) {
+                    double t[8];
 #pragma unroll
-                    for (int q = 0; q < K::P; ++q) t += (double)acc[q][b][r];
-                    *slot = t;
+                    for (int r = 0; r < 8; ++r)
+                        t[r] = acc64_lds[((wave * BM + b) * 16 + h + r) * 64 + lane];
+#pragma unroll
+                    for (int q = 0; q < K::P; ++q)
+#pragma unroll
+                        for (int r = 0; r < 8; ++r) t[r] += (double)acc[q][b][h + r];
+#pragma unroll
+                    for (int r = 0; r < 8; ++r)
+                        acc64_lds[((wave * BM + b) * 16 + h + r) * 64 + lane] = t[r];
                 }
         } else {
 #pragma unroll
