@@ -33,9 +33,12 @@ PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA (AMD published)
 PEAK_FP32_MATRIX = 157.3       # context: native FP32 matrix
 PEAK_FP64_MATRIX = 78.6        # context: native FP64 matrix/vector
 VARIANTS = [("sgemm", 6), ("dgemm", 6), ("dgemm", 10), ("dgemm", 15), ("dgemm", 21)]
+_CSRC = "paper_2609_04663_amd/csrc/"
+# sources a GEMM kernel is compiled from (a stored traffic figure is only used
+# while their hash is unchanged)
 KERNEL_SOURCES = {
-    "sgemm": "paper_2609_04663_amd/csrc/gemm_f32.hip",
-    "dgemm": "paper_2609_04663_amd/csrc/gemm_f64.hip",
+    "sgemm": [_CSRC + "gemm_f32.hip", _CSRC + "gemm_common.h", _CSRC + "emu_internal.h"],
+    "dgemm": [_CSRC + "gemm_f64.hip", _CSRC + "gemm_common.h", _CSRC + "emu_internal.h"],
 }
 
 
@@ -43,9 +46,12 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def source_hash(rel):
-    with open(os.path.join(ROOT, rel), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def source_hash(rels):
+    h = hashlib.sha256()
+    for rel in rels:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def traffic_for(kernel_key):
@@ -74,7 +80,15 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=2,
                     help="rows of C the oracle computes per variant for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="first run one plain device-to-device copy of this many MiB: the "
+                         "reference kernel that scales rocprofv3 FETCH_SIZE/WRITE_SIZE readings")
+    ap.add_argument("--print-source-hash", action="store_true",
+                    help="print the source hash of each GEMM kernel and exit")
     args = ap.parse_args()
+    if args.print_source_hash:
+        print(json.dumps({k: source_hash(v) for k, v in KERNEL_SOURCES.items()}))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(how the computation would shard is described in DESIGN.md).", file=sys.stderr)
@@ -86,6 +100,15 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.copy_calibration_mib > 0:
+        nbytes = args.copy_calibration_mib << 20
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"bench: calibration copy of {nbytes} bytes done")
+        del src, dst
     n = args.size
     log(f"bench: generating inputs M=N=K={n}")
     sa, sb = S.seeds(2)

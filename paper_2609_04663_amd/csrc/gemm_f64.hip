@@ -264,7 +264,7 @@ hipError_t launch_gemm_f64(const uint16_t *Ap, const uint16_t *Bp, double *C, in
     switch (d) {
         case 3: return launch_t<3, 2, 3, false>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, s);
         case 4: return launch_t<4, 1, 3, false>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, s);
-        case 5: return launch_t<5, 1, 3, false>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, s);
+        case 5: return launch_t<5, 1, 3, true>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, s);
         case 6: return launch_t<6, 1, 2, true>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, s);
         default: return hipErrorInvalidValue;
     }
