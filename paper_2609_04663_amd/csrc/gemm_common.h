@@ -3,6 +3,8 @@
 
 #include "emu_internal.h"
 
+#include <utility>
+
 namespace emu {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -78,6 +80,22 @@ __device__ inline void pipeline_barrier() {
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
 }
+
+// f(std::integral_constant<int, I>) for I = 0 .. N - 1, in order, with I a
+// constant expression inside f (for instruction sequences fixed at compile time).
+template <typename F, int... I>
+__device__ inline void static_for_impl(F &f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ inline void static_for(F &&f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// Scheduling fence that lets only VALU and SALU instructions (address
+// arithmetic) move across it: MFMA, LDS and global memory instructions keep
+// their program order.
+__device__ inline void order_fence() { __builtin_amdgcn_sched_barrier(0x6); }
 
 // Output coordinates of accumulator register r of lane l in a 32x32 block:
 // row (r / 4) * 8 + (l / 32) * 4 + r % 4, column l % 32.
