@@ -32,6 +32,15 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA (AMD published)
 PEAK_FP32_MATRIX = 157.3       # context: native FP32 matrix
 PEAK_FP64_MATRIX = 78.6        # context: native FP64 matrix/vector
+# The paper's own figures at m = n = k = 8192 (Figs. fullcore-fp32 and
+# fullcore-fp64: 2 x Xeon Platinum 8462Y+, AMX-BF16, 64 threads, oneMKL 2026.1
+# baselines), as printed; another machine, context only.
+PAPER_CONTEXT_8192 = {
+    "machine": "2x Intel Xeon Platinum 8462Y+ (AMX-BF16), 64 threads; values as printed in the "
+               "paper's Figs. fullcore-fp32/fullcore-fp64 (axis labelled GFLOPS)",
+    "emu_sgemm": 11.174, "mkl_sgemm": 9.603,
+    "emu_dgemm": {"6": 6.787, "10": 4.543, "15": 3.224, "21": 2.359}, "mkl_dgemm": 4.887,
+}
 VARIANTS = [("sgemm", 6), ("dgemm", 6), ("dgemm", 10), ("dgemm", 15), ("dgemm", 21)]
 _CSRC = "paper_2609_04663_amd/csrc/"
 # sources a GEMM kernel is compiled from (a stored traffic figure is only used
@@ -77,12 +86,14 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--size", type=int, default=8192, help="M = N = K")
-    ap.add_argument("--cpu-rows", type=int, default=2,
+    ap.add_argument("--cpu-rows", type=int, default=4,
                     help="rows of C the oracle computes per variant for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run one plain device-to-device copy of this many MiB: the "
                          "reference kernel that scales rocprofv3 FETCH_SIZE/WRITE_SIZE readings")
+    ap.add_argument("--no-native", action="store_true",
+                    help="skip timing the vendor library's native FP32/FP64 GEMM (context)")
     ap.add_argument("--print-source-hash", action="store_true",
                     help="print the source hash of each GEMM kernel and exit")
     args = ap.parse_args()
@@ -146,6 +157,24 @@ def main():
     status = emu.domain_status()
     assert len(split_ms) == len(VARIANTS) * args.steps, "profile pool too small"
 
+    # context: the vendor library's native FP32 and FP64 GEMM on the same inputs
+    native = None
+    if not args.no_native:
+        def lib_rate(a, b, reps):
+            c = a @ b
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                c = a @ b
+            e1.record()
+            torch.cuda.synchronize()
+            return 2.0 * n ** 3 / (e0.elapsed_time(e1) / reps * 1e-3) / 1e12
+        log("bench: native FP32/FP64 GEMM (vendor library) for context")
+        native = {"fp32_tflops": round(lib_rate(dA32, dB32, 3), 2),
+                  "fp64_tflops": round(lib_rate(dA64, dB64, 2), 2),
+                  "library": "torch.matmul (hipBLASLt/rocBLAS), same inputs"}
+
     flop = 2.0 * n ** 3
     elapsed = t1 - t0
     value = len(VARIANTS) * flop * args.steps / elapsed / 1e12
@@ -154,13 +183,24 @@ def main():
         s = np.array(split_ms[vi::len(VARIANTS)])
         g = np.array(gemm_ms[vi::len(VARIANTS)])
         name = "emu-SGEMM" if kind == "sgemm" else f"emu-DGEMM-{p}"
+        # split/pack pass, algorithmic bytes: both operands read once, their
+        # BF16 planes (3, or d = 3..6 slices) written once
+        in_bytes, planes = (4, 3) if kind == "sgemm" else (8, {6: 3, 10: 4, 15: 5, 21: 6}[p])
+        split_bytes = (in_bytes + 2 * planes) * 2.0 * n * n
         per_variant[name] = {
             "effective_tflops": round(flop / ((s.mean() + g.mean()) * 1e-3) / 1e12, 2),
             "split_ms": round(float(s.mean()), 4),
             "gemm_ms": round(float(g.mean()), 4),
             "split_share": round(float(s.mean() / (s.mean() + g.mean())), 4),
+            "split_gbps": round(split_bytes / (s.mean() * 1e-3) / 1e9, 1),
             "mfma_frac": round(p * flop / (g.mean() * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         }
+    if native:
+        native["emu_sgemm_speedup_vs_native_fp32"] = round(
+            per_variant["emu-SGEMM"]["effective_tflops"] / native["fp32_tflops"], 3)
+        native["emu_dgemm_speedup_vs_native_fp64"] = {
+            str(p): round(per_variant[f"emu-DGEMM-{p}"]["effective_tflops"] / native["fp64_tflops"], 3)
+            for p in (6, 10, 15, 21)}
     # dominant kernel: the GEMM launch with the largest share of the step
     dom = max(range(len(VARIANTS)), key=lambda i: np.mean(gemm_ms[i::len(VARIANTS)]))
     kind, p = VARIANTS[dom]
@@ -235,6 +275,8 @@ def main():
         "domain_status": status,
         "context_peaks_tflops": {"bf16_mfma": PEAK_BF16_TFLOPS, "fp32_matrix": PEAK_FP32_MATRIX,
                                  "fp64_matrix": PEAK_FP64_MATRIX},
+        "context_native_gemm": native,
+        "context_paper_8192": PAPER_CONTEXT_8192 if n == 8192 else None,
     }
     print(json.dumps(line), flush=True)
 

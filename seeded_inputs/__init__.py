@@ -25,71 +25,114 @@ Distributions (all computed in FP64; FP32 operands are one RNE cast of that):
   2**16; the rows are the first entries of a seeded Fisher-Yates permutation.
 
 Seeds: operand A of workload ``cfg`` uses ``1000*cfg + 1`` and B ``1000*cfg + 2``.
+
+The bulk loops run in ``gen.c`` (built on first use with gcc into ``_gen.so``,
+or by ``build()``); ``stream`` and ``element`` are also written out in plain
+Python for checking it.
 """
 from __future__ import annotations
 
+import ctypes
 import hashlib
+import math
+import os
+import subprocess
 
 import numpy as np
 
-_GAMMA = np.uint64(0x9E3779B97F4A7C15)
-_M1 = np.uint64(0xBF58476D1CE4E5B9)
-_M2 = np.uint64(0x94D049BB133111EB)
-_CHUNK = 1 << 22
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SO = os.path.join(_HERE, "_gen.so")
+_lib = None
 
 
-def _mix64(z: np.ndarray) -> np.ndarray:
-    """SplitMix64 output function (Steele, Lea, Flood 2014), on uint64 arrays."""
-    z = z.copy()
-    z ^= z >> np.uint64(30)
-    z *= _M1
-    z ^= z >> np.uint64(27)
-    z *= _M2
-    z ^= z >> np.uint64(31)
-    return z
+def build(force: bool = False) -> str:
+    """Compile gen.c into _gen.so (gcc, OpenMP, no FP contraction)."""
+    src = os.path.join(_HERE, "gen.c")
+    if force or not os.path.exists(_SO) or os.path.getmtime(_SO) < os.path.getmtime(src):
+        tmp = _SO + f".tmp{os.getpid()}"
+        subprocess.run(["gcc", "-O2", "-fopenmp", "-ffp-contract=off", "-fno-fast-math", "-fPIC",
+                        "-shared", src, "-o", tmp, "-lm"], check=True)
+        os.replace(tmp, _SO)
+    return _SO
+
+
+def _gen():
+    global _lib
+    if _lib is None:
+        L = ctypes.CDLL(build())
+        u64, i64, p, d, ci = (ctypes.c_uint64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_double,
+                              ctypes.c_int)
+        L.sg_stream.argtypes = [u64, i64, i64, p]
+        L.sg_uniform.argtypes = [u64, i64, d, d, p]
+        L.sg_normal.argtypes = [u64, i64, p]
+        L.sg_wide.argtypes = [u64, i64, ci, ci, p]
+        for f in (L.sg_stream, L.sg_uniform, L.sg_normal, L.sg_wide):
+            f.restype = None
+        _lib = L
+    return _lib
+
+
+def _u64(seed: int) -> int:
+    return int(seed) % (1 << 64)
 
 
 def stream(seed: int, n: int, offset: int = 0) -> np.ndarray:
     """Elements ``offset .. offset+n-1`` of counter-based stream ``seed`` (uint64)."""
     out = np.empty(n, dtype=np.uint64)
-    base = (int(seed) << 32) + int(offset) + 1
-    with np.errstate(over="ignore"):
-        for s in range(0, n, _CHUNK):
-            e = min(n, s + _CHUNK)
-            ctr = (np.arange(s, e, dtype=np.uint64) + np.uint64(base % (1 << 64)))
-            out[s:e] = _mix64(ctr * _GAMMA)
+    if n:
+        _gen().sg_stream(_u64(seed), n, int(offset), out.ctypes.data)
     return out
 
 
-def _unit53(x: np.ndarray) -> np.ndarray:
-    return (x >> np.uint64(11)).astype(np.float64) * 2.0 ** -53
+def element(seed: int, i: int) -> int:
+    """Element ``i`` of stream ``seed`` in plain Python integers (the definition)."""
+    mask = (1 << 64) - 1
+    z = ((((int(seed) << 32) + i + 1) & mask) * 0x9E3779B97F4A7C15) & mask
+    z ^= z >> 30
+    z = (z * 0xBF58476D1CE4E5B9) & mask
+    z ^= z >> 27
+    z = (z * 0x94D049BB133111EB) & mask
+    return z ^ (z >> 31)
 
 
 def uniform(seed: int, shape, lo: float = -1.0, hi: float = 1.0) -> np.ndarray:
     n = int(np.prod(shape))
-    u = _unit53(stream(seed, n))
-    return (lo + (hi - lo) * u).reshape(shape)
+    out = np.empty(n, dtype=np.float64)
+    if n:
+        _gen().sg_uniform(_u64(seed), n, float(lo), float(hi), out.ctypes.data)
+    return out.reshape(shape)
 
 
 def normal(seed: int, shape) -> np.ndarray:
     n = int(np.prod(shape))
-    x = stream(seed, 2 * n)
-    u1 = ((x[0::2] >> np.uint64(11)).astype(np.float64) + 1.0) * 2.0 ** -53
-    u2 = _unit53(x[1::2])
-    return (np.sqrt(-2.0 * np.log(u1)) * np.cos(2.0 * np.pi * u2)).reshape(shape)
+    out = np.empty(n, dtype=np.float64)
+    if n:
+        _gen().sg_normal(_u64(seed), n, out.ctypes.data)
+    return out.reshape(shape)
 
 
 def wide(seed: int, shape, emin: int = -20, emax: int = 20) -> np.ndarray:
     n = int(np.prod(shape))
-    x = stream(seed, 2 * n)
-    x0, x1 = x[0::2], x[1::2]
-    sign = np.where((x0 & np.uint64(1)) == 0, 1.0, -1.0)
-    span = np.uint64(emax - emin + 1)
-    with np.errstate(over="ignore"):
-        e = ((x0 >> np.uint64(32)) * span) >> np.uint64(32)
-    e = e.astype(np.int64) + emin
-    m = 1.0 + (x1 >> np.uint64(12)).astype(np.float64) * 2.0 ** -52
-    return np.ldexp(sign * m, e.astype(np.int32)).reshape(shape)
+    out = np.empty(n, dtype=np.float64)
+    if n:
+        _gen().sg_wide(_u64(seed), n, int(emin), int(emax), out.ctypes.data)
+    return out.reshape(shape)
+
+
+def value(dist: str, seed: int, i: int) -> float:
+    """Element ``i`` of a distribution, in plain Python (checks the bulk loops)."""
+    if dist == "uniform":
+        return -1.0 + 2.0 * ((element(seed, i) >> 11) * 2.0 ** -53)
+    x0, x1 = element(seed, 2 * i), element(seed, 2 * i + 1)
+    if dist == "normal":
+        u1 = ((x0 >> 11) + 1.0) * 2.0 ** -53
+        u2 = (x1 >> 11) * 2.0 ** -53
+        return math.sqrt(-2.0 * math.log(u1)) * math.cos(2.0 * math.pi * u2)
+    if dist == "wide":
+        s = -1.0 if x0 & 1 else 1.0
+        e = (((x0 >> 32) * 41) >> 32) - 20
+        return math.ldexp(s * (1.0 + (x1 >> 12) * 2.0 ** -52), e)
+    raise ValueError(dist)
 
 
 def permutation(seed: int, n: int) -> np.ndarray:
