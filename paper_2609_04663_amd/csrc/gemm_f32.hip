@@ -50,25 +50,23 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
 
     // Copy issue for one k-block: wave w moves 1 KB parts [3w, 3w + 3) of each A
     // plane and [2w, 2w + 2) of each B plane, so every address is a wave-uniform
-    // base plus a compile-time offset.
+    // base plus a compile-time offset.  Copy j < 9 is A plane j / 3, part j % 3;
+    // copy 9 + j is B plane j / 2, part j % 2.
     static_assert(A_BYTES / 1024 == 12 && B_BYTES / 1024 == 8, "part split assumes 192 x 128");
+    constexpr int COPIES = 15;
     const int64_t a_base = m0 * 64 + wave * 3 * 1024;
     const int64_t b_base = n0 * 64 + wave * 2 * 1024;
-    auto issue = [&](int kb, char *base) {
-        const char *a_src = Ag + (int64_t)kb * RpadA * 64 + a_base;
-        const char *b_src = Bg + (int64_t)kb * RpadB * 64 + b_base;
-        char *a_dst = base + wave * 3 * 1024;
-        char *b_dst = base + NC * A_BYTES + wave * 2 * 1024;
-#pragma unroll
-        for (int c = 0; c < NC; ++c)
-#pragma unroll
-            for (int j = 0; j < 3; ++j)
-                copy_1k(a_src + c * a_plane + j * 1024, a_dst + c * A_BYTES + j * 1024, lane);
-#pragma unroll
-        for (int c = 0; c < NC; ++c)
-#pragma unroll
-            for (int j = 0; j < 2; ++j)
-                copy_1k(b_src + c * b_plane + j * 1024, b_dst + c * B_BYTES + j * 1024, lane);
+    auto issue_one = [&](int kb, char *base, auto j_c) {
+        constexpr int j = decltype(j_c)::value;
+        if constexpr (j < 9)
+            copy_1k(Ag + (int64_t)kb * RpadA * 64 + a_base + (j / 3) * a_plane + (j % 3) * 1024,
+                    base + wave * 3 * 1024 + (j / 3) * A_BYTES + (j % 3) * 1024, lane);
+        else
+            copy_1k(Bg + (int64_t)kb * RpadB * 64 + b_base + ((j - 9) / 2) * b_plane +
+                        ((j - 9) % 2) * 1024,
+                    base + NC * A_BYTES + wave * 2 * 1024 + ((j - 9) / 2) * B_BYTES +
+                        ((j - 9) % 2) * 1024,
+                    lane);
     };
 
     const int off0 = frag_offset(lane, 0), off1 = frag_offset(lane, 1);
@@ -79,44 +77,53 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
         bf16x8 b[NC][2];
         bf16x8 a[NC][RB];
     };
+    const int at0 = (wm * 32 * RB) * 64, bt0 = NC * A_BYTES + (wn * 64) * 64;
     auto load = [&](const char *base, int off, Frags &f) {
-        const char *At = base + (wm * 32 * RB) * 64;
-        const char *Bt = base + NC * A_BYTES + (wn * 64) * 64;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
 #pragma unroll
-            for (int cb = 0; cb < 2; ++cb) f.b[c][cb] = lds_frag(Bt + c * B_BYTES + cb * 32 * 64, off);
+            for (int cb = 0; cb < 2; ++cb) f.b[c][cb] = lds_frag(base + bt0 + c * B_BYTES + cb * 32 * 64, off);
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb) f.a[c][rb] = lds_frag(At + c * A_BYTES + rb * 32 * 64, off);
+            for (int rb = 0; rb < RB; ++rb) f.a[c][rb] = lds_frag(base + at0 + c * A_BYTES + rb * 32 * 64, off);
         }
     };
-    // The six products on one sub-step: A0B0 into hi, A0B1 A0B2 A1B0 A1B1 A2B0
-    // into lo.  zero: the panel's first sub-step (accumulators start at 0).
-    auto mma = [&](const Frags &f, f32x16 (&hi)[RB][2], f32x16 (&lo)[RB][2], bool zero) {
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb)
-                hi[rb][cb] = mfma(f.a[0][rb], f.b[0][cb], zero ? f32x16{} : hi[rb][cb]);
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb)
-                lo[rb][cb] = mfma(f.a[0][rb], f.b[1][cb], zero ? f32x16{} : lo[rb][cb]);
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb) lo[rb][cb] = mfma(f.a[0][rb], f.b[2][cb], lo[rb][cb]);
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-                for (int cb = 0; cb < 2; ++cb) lo[rb][cb] = mfma(f.a[1][rb], f.b[j][cb], lo[rb][cb]);
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb) lo[rb][cb] = mfma(f.a[2][rb], f.b[0][cb], lo[rb][cb]);
+    // One sub-step in slots of one MFMA, one fragment read of the next sub-step
+    // and one copy (MFMA first: its operands were read a sub-step earlier).
+    // MFMA t is product t / 6 of (A0B0 | A0B1 A0B2 A1B0 A1B1 A2B0) on block
+    // (rb, cb) = ((t % 6) / 2, t % 2): A0B0 goes to hi, the five smaller products
+    // to lo, product-major so that consecutive MFMAs never share an accumulator.
+    // Read t fetches fragments in order of first use: A0, B0, B1, B2, A1, A2.
+    // zero: the panel's first sub-step (accumulators start at 0).
+    constexpr int PI[6] = {0, 0, 0, 1, 1, 2}, PJ[6] = {0, 1, 2, 0, 1, 0};
+    auto step = [&](const Frags &cur, f32x16 (&hi)[RB][2], f32x16 (&lo)[RB][2], auto zero_c,
+                    const char *nbase, int noff, Frags &nxt, int ckb, char *cdst, auto ncopy_c) {
+        constexpr bool zero = decltype(zero_c)::value;
+        constexpr int NCOPY = decltype(ncopy_c)::value;
+        static_for<6 * RB * 2>([&](auto t_c) {
+            constexpr int t = decltype(t_c)::value;
+            constexpr int g = t / (RB * 2), rb = (t % (RB * 2)) / 2, cb = t % 2;
+            constexpr int i = PI[g], j = PJ[g];
+            if constexpr (g == 0)
+                hi[rb][cb] = mfma(cur.a[0][rb], cur.b[0][cb], zero ? f32x16{} : hi[rb][cb]);
+            else
+                lo[rb][cb] = mfma(cur.a[i][rb], cur.b[j][cb], (zero && g == 1) ? f32x16{} : lo[rb][cb]);
+            order_fence();
+            if constexpr (t < 15) {
+                // A0 (RB), B0 B1 B2 (2 each), A1 (RB), A2 (RB)
+                if constexpr (t < RB)
+                    nxt.a[0][t] = lds_frag(nbase + at0 + t * 32 * 64, noff);
+                else if constexpr (t < RB + 6)
+                    nxt.b[(t - RB) / 2][(t - RB) % 2] =
+                        lds_frag(nbase + bt0 + ((t - RB) / 2) * B_BYTES + ((t - RB) % 2) * 32 * 64, noff);
+                else
+                    nxt.a[1 + (t - RB - 6) / RB][(t - RB - 6) % RB] =
+                        lds_frag(nbase + at0 + (1 + (t - RB - 6) / RB) * A_BYTES +
+                                     ((t - RB - 6) % RB) * 32 * 64, noff);
+            }
+            order_fence();
+            if constexpr (t < NCOPY) issue_one(ckb, cdst, std::integral_constant<int, t>{});
+            order_fence();
+        });
     };
 
     f32x16 blk[RB][2];
@@ -132,9 +139,10 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
     // reads, then barriers: now every wave is done reading stage kb and every
     // copy of kb + 1 has landed; (3) starts the copy of kb + 2 into stage kb and
     // reads the sub-step-0 fragments of kb + 1 while the sub-step-1 MFMAs run.
-    issue(0, stage0);
-    if (KB > 1) issue(1, stage1);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // The copy past the last k-block re-reads the last one (in bounds, unused).
+    static_for<COPIES>([&](auto j_c) { issue_one(0, stage0, j_c); });
+    static_for<COPIES>([&](auto j_c) { issue_one(min(1, KB - 1), stage1, j_c); });
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(COPIES) : "memory");
     __syncthreads();
     Frags f0, f1;
     load(stage0, off0, f0);
@@ -142,37 +150,19 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
     for (int p0 = 0; p0 < KB; p0 += KB_PER_PANEL) {
         const int p1 = min(KB, p0 + KB_PER_PANEL);
         f32x16 hi[RB][2], lo[RB][2];
-        auto kblock = [&](bool first) {
+        auto kblock = [&](auto first_c) {
             char *cur = (kb & 1) ? stage1 : stage0;
             char *nxt = (kb & 1) ? stage0 : stage1;
-            load(cur, off1, f1);
-            mma(f0, hi, lo, first);
-            // 15 fragment reads spread over the 36 MFMAs of sub-step 0
-#pragma unroll
-            for (int i = 0; i < 15; ++i) {
-                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
-                __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // MFMA
-            }
-            __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
+            step(f0, hi, lo, first_c, cur, off1, f1, 0, cur, std::integral_constant<int, 0>{});
             __builtin_amdgcn_sched_barrier(0);
             asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
             pipeline_barrier();
-            // the copy past the last k-block re-reads the last one (in bounds, unused)
-            issue(min(kb + 2, KB - 1), cur);
-            load(nxt, off0, f0);      // unused after the last k-block; always in bounds
-            mma(f1, hi, lo, false);
-            // 15 copies and 15 fragment reads spread over the 36 MFMAs of sub-step 1
-#pragma unroll
-            for (int i = 0; i < 15; ++i) {
-                __builtin_amdgcn_sched_group_barrier(0x020, 1, 1);   // VMEM read (copy)
-                __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);   // DS read
-                __builtin_amdgcn_sched_group_barrier(0x008, 2, 1);   // MFMA
-            }
-            __builtin_amdgcn_sched_group_barrier(0x008, 6, 1);
+            step(f1, hi, lo, std::false_type{}, nxt, off0, f0, min(kb + 2, KB - 1), cur,
+                 std::integral_constant<int, COPIES>{});
             __builtin_amdgcn_sched_barrier(0);
         };
-        kblock(true);                 // panel's first k-block: accumulators start at 0
-        for (++kb; kb < p1; ++kb) kblock(false);
+        kblock(std::true_type{});     // panel's first k-block: accumulators start at 0
+        for (++kb; kb < p1; ++kb) kblock(std::false_type{});
 #pragma unroll
         for (int i = 0; i < RB; ++i)
 #pragma unroll
