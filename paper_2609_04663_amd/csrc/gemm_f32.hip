@@ -71,57 +71,58 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
 
     const int off0 = frag_offset(lane, 0), off1 = frag_offset(lane, 1);
 
-    // Fragments of one 16-index sub-step: the three B planes (2 column blocks)
-    // and the three A planes (RB row blocks).
+    // Operand fragments of one 16-index sub-step: the three B planes (2 column
+    // blocks) and the three A planes (RB row blocks).  One register set: each
+    // fragment is re-read for the next sub-step right after its last use in the
+    // current one, except B0, whose last use is the sub-step's last MFMA: it has
+    // a second buffer (b0 below) that is filled at the start of the sub-step.
     struct Frags {
         bf16x8 b[NC][2];
         bf16x8 a[NC][RB];
     };
     const int at0 = (wm * 32 * RB) * 64, bt0 = NC * A_BYTES + (wn * 64) * 64;
-    auto load = [&](const char *base, int off, Frags &f) {
-#pragma unroll
-        for (int c = 0; c < NC; ++c) {
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb) f.b[c][cb] = lds_frag(base + bt0 + c * B_BYTES + cb * 32 * 64, off);
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb) f.a[c][rb] = lds_frag(base + at0 + c * A_BYTES + rb * 32 * 64, off);
-        }
+    auto read_a = [&](const char *base, int off, int c, int rb) {
+        return lds_frag(base + at0 + c * A_BYTES + rb * 32 * 64, off);
     };
-    // One sub-step in slots of one MFMA, one fragment read of the next sub-step
-    // and one copy (MFMA first: its operands were read a sub-step earlier).
-    // MFMA t is product t / 6 of (A0B0 | A0B1 A0B2 A1B0 A1B1 A2B0) on block
-    // (rb, cb) = ((t % 6) / 2, t % 2): A0B0 goes to hi, the five smaller products
-    // to lo, product-major so that consecutive MFMAs never share an accumulator.
-    // Read t fetches fragments in order of first use: A0, B0, B1, B2, A1, A2.
+    auto read_b = [&](const char *base, int off, int c, int cb) {
+        return lds_frag(base + bt0 + c * B_BYTES + cb * 32 * 64, off);
+    };
+    // One sub-step in 36 slots.  MFMA t is product g = t / 6 of
+    // (A0B0 | A0B1 A0B2 A1B0 A1B1 A2B0) on block (rb, cb) = ((t % 6) / 2, t % 2):
+    // A0B0 goes to hi, the five smaller products to lo, product-major so that
+    // consecutive MFMAs never share an accumulator.  After MFMA t come the reads
+    // of the next sub-step (stage nbase, lane offset noff) of the fragments whose
+    // last use was MFMA t, then copy t / 2 of k-block ckb (even t, t / 2 < NCOPY).
+    // Latency cover of every read: at least 12 MFMAs.
     // zero: the panel's first sub-step (accumulators start at 0).
     constexpr int PI[6] = {0, 0, 0, 1, 1, 2}, PJ[6] = {0, 1, 2, 0, 1, 0};
-    auto step = [&](const Frags &cur, f32x16 (&hi)[RB][2], f32x16 (&lo)[RB][2], auto zero_c,
-                    const char *nbase, int noff, Frags &nxt, int ckb, char *cdst, auto ncopy_c) {
+    auto step = [&](Frags &f, const bf16x8 (&b0)[2], bf16x8 (&b0n)[2], f32x16 (&hi)[RB][2],
+                    f32x16 (&lo)[RB][2], auto zero_c, const char *nbase, int noff, int ckb,
+                    char *cdst, auto ncopy_c) {
         constexpr bool zero = decltype(zero_c)::value;
         constexpr int NCOPY = decltype(ncopy_c)::value;
-        static_for<6 * RB * 2>([&](auto t_c) {
+        static_assert(RB == 3, "last-use slots below assume three row blocks");
+        static_for<36>([&](auto t_c) {
             constexpr int t = decltype(t_c)::value;
-            constexpr int g = t / (RB * 2), rb = (t % (RB * 2)) / 2, cb = t % 2;
+            constexpr int g = t / 6, rb = (t % 6) / 2, cb = t % 2;
             constexpr int i = PI[g], j = PJ[g];
+            const bf16x8 &bop = (j == 0) ? b0[cb] : f.b[j][cb];
             if constexpr (g == 0)
-                hi[rb][cb] = mfma(cur.a[0][rb], cur.b[0][cb], zero ? f32x16{} : hi[rb][cb]);
+                hi[rb][cb] = mfma(f.a[0][rb], bop, zero ? f32x16{} : hi[rb][cb]);
             else
-                lo[rb][cb] = mfma(cur.a[i][rb], cur.b[j][cb], (zero && g == 1) ? f32x16{} : lo[rb][cb]);
+                lo[rb][cb] = mfma(f.a[i][rb], bop, (zero && g == 1) ? f32x16{} : lo[rb][cb]);
             order_fence();
-            if constexpr (t < 15) {
-                // A0 (RB), B0 B1 B2 (2 each), A1 (RB), A2 (RB)
-                if constexpr (t < RB)
-                    nxt.a[0][t] = lds_frag(nbase + at0 + t * 32 * 64, noff);
-                else if constexpr (t < RB + 6)
-                    nxt.b[(t - RB) / 2][(t - RB) % 2] =
-                        lds_frag(nbase + bt0 + ((t - RB) / 2) * B_BYTES + ((t - RB) % 2) * 32 * 64, noff);
-                else
-                    nxt.a[1 + (t - RB - 6) / RB][(t - RB - 6) % RB] =
-                        lds_frag(nbase + at0 + (1 + (t - RB - 6) / RB) * A_BYTES +
-                                     ((t - RB - 6) % RB) * 32 * 64, noff);
-            }
+            // last uses: B0 -> second buffer at t = 0, 1; A0[r] at 13 + 2r; B2[c] at
+            // 16 + c; A1[r] at 25 + 2r; B1[c] at 28 + c; A2[r] at 31 + 2r
+            if constexpr (t < 2) b0n[t] = read_b(nbase, noff, 0, t);
+            if constexpr (t == 13 || t == 15 || t == 17) f.a[0][(t - 13) / 2] = read_a(nbase, noff, 0, (t - 13) / 2);
+            if constexpr (t == 16 || t == 17) f.b[2][t - 16] = read_b(nbase, noff, 2, t - 16);
+            if constexpr (t == 25 || t == 27 || t == 29) f.a[1][(t - 25) / 2] = read_a(nbase, noff, 1, (t - 25) / 2);
+            if constexpr (t == 28 || t == 29) f.b[1][t - 28] = read_b(nbase, noff, 1, t - 28);
+            if constexpr (t == 31 || t == 33 || t == 35) f.a[2][(t - 31) / 2] = read_a(nbase, noff, 2, (t - 31) / 2);
             order_fence();
-            if constexpr (t < NCOPY) issue_one(ckb, cdst, std::integral_constant<int, t>{});
+            if constexpr (t % 2 == 0 && t / 2 < NCOPY)
+                issue_one(ckb, cdst, std::integral_constant<int, t / 2>{});
             order_fence();
         });
     };
@@ -144,8 +145,17 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
     static_for<COPIES>([&](auto j_c) { issue_one(min(1, KB - 1), stage1, j_c); });
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(COPIES) : "memory");
     __syncthreads();
-    Frags f0, f1;
-    load(stage0, off0, f0);
+    Frags f;
+    bf16x8 b0a[2], b0b[2];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb) f.b[c][cb] = read_b(stage0, off0, c, cb);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) f.a[c][rb] = read_a(stage0, off0, c, rb);
+    }
+    b0a[0] = f.b[0][0];
+    b0a[1] = f.b[0][1];
     int kb = 0;
     for (int p0 = 0; p0 < KB; p0 += KB_PER_PANEL) {
         const int p1 = min(KB, p0 + KB_PER_PANEL);
@@ -153,11 +163,11 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
         auto kblock = [&](auto first_c) {
             char *cur = (kb & 1) ? stage1 : stage0;
             char *nxt = (kb & 1) ? stage0 : stage1;
-            step(f0, hi, lo, first_c, cur, off1, f1, 0, cur, std::integral_constant<int, 0>{});
+            step(f, b0a, b0b, hi, lo, first_c, cur, off1, 0, cur, std::integral_constant<int, 0>{});
             __builtin_amdgcn_sched_barrier(0);
             asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
             pipeline_barrier();
-            step(f1, hi, lo, std::false_type{}, nxt, off0, f0, min(kb + 2, KB - 1), cur,
+            step(f, b0b, b0a, hi, lo, std::false_type{}, nxt, off0, min(kb + 2, KB - 1), cur,
                  std::integral_constant<int, COPIES>{});
             __builtin_amdgcn_sched_barrier(0);
         };
