@@ -29,9 +29,15 @@ __device__ inline void tile_coords(int nt_m, int nt_n, int &tm, int &tn) {
 }
 
 // One 1 KB direct global->LDS copy by a wave: lane l moves 16 bytes from
-// src + 16 l to lds_dst + 16 l (lds_dst must be uniform over the wave).
-__device__ inline void copy_1k(const char *src_wave, char *lds_dst, int lane) {
-    __builtin_amdgcn_global_load_lds((const void *)(src_wave + lane * 16), (lds_void_ptr)lds_dst, 16,
+// src_wave + 16 l to lds_dst + 16 l (src_wave and lds_dst must be uniform over
+// the wave).  The source base is pinned to scalar registers so that the copy
+// takes the scalar-base form (64-bit base in SGPRs, 32-bit lane offset in one
+// VGPR shared by every copy) instead of a 64-bit address per lane; that form
+// holds the issuing wave for fewer cycles.
+__device__ inline void copy_1k(const char *src_wave, char *lds_dst, unsigned lane16) {
+    asm volatile("" : "+s"(src_wave));
+    asm volatile("" : "+v"(lane16));   // keeps the offset 32-bit at the copy (no hoisted widening)
+    __builtin_amdgcn_global_load_lds((const void *)(src_wave + lane16), (lds_void_ptr)lds_dst, 16,
                                      0, 0);
 }
 

@@ -39,6 +39,7 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
     int tm, tn;
     tile_coords<4>(nt_m, nt_n, tm, tn);
     const int lane = threadIdx.x & 63;
+    const unsigned lane16 = (unsigned)lane * 16u;   // copy offset of this lane
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
     const int wm = wave >> 1, wn = wave & 1;
     const int64_t m0 = (int64_t)tm * MT, n0 = (int64_t)tn * NT;
@@ -60,13 +61,13 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
         constexpr int j = decltype(j_c)::value;
         if constexpr (j < 9)
             copy_1k(Ag + (int64_t)kb * RpadA * 64 + a_base + (j / 3) * a_plane + (j % 3) * 1024,
-                    base + wave * 3 * 1024 + (j / 3) * A_BYTES + (j % 3) * 1024, lane);
+                    base + wave * 3 * 1024 + (j / 3) * A_BYTES + (j % 3) * 1024, lane16);
         else
             copy_1k(Bg + (int64_t)kb * RpadB * 64 + b_base + ((j - 9) / 2) * b_plane +
                         ((j - 9) % 2) * 1024,
                     base + NC * A_BYTES + wave * 2 * 1024 + ((j - 9) / 2) * B_BYTES +
                         ((j - 9) % 2) * 1024,
-                    lane);
+                    lane16);
     };
 
     const int off0 = frag_offset(lane, 0), off1 = frag_offset(lane, 1);

@@ -92,6 +92,7 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
     int tm, tn;
     tile_coords<8>(nt_m, nt_n, tm, tn);
     const int lane = threadIdx.x & 63;
+    const unsigned lane16 = (unsigned)lane * 16u;   // copy offset of this lane
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
     const int wm = wave >> 1, wn = wave & 1;
     const int64_t m0 = (int64_t)tm * K::MT, n0 = (int64_t)tn * K::NT;
@@ -112,10 +113,10 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
         constexpr int j = decltype(j_c)::value, c = j / (BM + 1), r = j % (BM + 1);
         if constexpr (r < BM)
             copy_1k(Ag + (int64_t)kb * RpadA * 64 + a_base + c * a_plane + r * 1024,
-                    base + wave * BM * 1024 + c * K::A_BYTES + r * 1024, lane);
+                    base + wave * BM * 1024 + c * K::A_BYTES + r * 1024, lane16);
         else
             copy_1k(Bg + (int64_t)kb * RpadB * 64 + b_base + c * b_plane,
-                    base + D * K::A_BYTES + wave * 1024 + c * K::B_BYTES, lane);
+                    base + D * K::A_BYTES + wave * 1024 + c * K::B_BYTES, lane16);
     };
     auto issue_all = [&](int kb, char *base) {
         static_for<K::COPIES>([&](auto j_c) { issue_one(kb, base, j_c); });
