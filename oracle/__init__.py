@@ -20,6 +20,7 @@ Functions (all operands row-major numpy arrays, all on the host):
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 import subprocess
@@ -38,53 +39,77 @@ ST_NAN, ST_RANGE, ST_SUBNORMAL, ST_OVERFLOW, ST_INEXACT32 = 1, 2, 4, 8, 16
 NPROD_TO_D = {6: 3, 10: 4, 15: 5, 21: 6}
 
 
+def compile_source(src: str, out: str) -> str:
+    """Compile a C source file into the shared library ``out`` with the oracle's
+    flags (no fast-math, no FMA contraction)."""
+    tmp = out + ".tmp%d" % os.getpid()
+    cmd = ["gcc", "-O2", "-fopenmp", "-ffp-contract=off", "-fno-fast-math", "-std=c11",
+           "-Wall", "-shared", "-fPIC", src, "-o", tmp, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, out)
+    return out
+
+
 def build(force: bool = True) -> str:
-    """Compile oracle.c with gcc (no fast-math, no FMA contraction)."""
+    """Compile oracle.c into liboracle.so."""
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-        tmp = _LIB + ".tmp%d" % os.getpid()
-        cmd = ["gcc", "-O2", "-fopenmp", "-ffp-contract=off", "-fno-fast-math", "-std=c11",
-               "-Wall", "-shared", "-fPIC", _SRC, "-o", tmp, "-lm"]
-        subprocess.run(cmd, check=True)
-        os.replace(tmp, _LIB)
+        compile_source(_SRC, _LIB)
     return _LIB
 
 
 _lib = None
 
 
+@contextlib.contextmanager
+def using_library(path: str):
+    """Route every call of this module through another build of the oracle
+    (the mutation tests use it to show that the pins reject planted mistakes)."""
+    global _lib
+    saved = _lib
+    _lib = _configure(ctypes.CDLL(os.path.abspath(path)))
+    try:
+        yield
+    finally:
+        _lib = saved
+
+
 def lib():
     global _lib
     if _lib is None:
         build(force=False)
-        L = ctypes.CDLL(_LIB)
-        i64, p, u32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_uint32
-        L.orc_bf16_rne_f32.argtypes = [ctypes.c_float]
-        L.orc_bf16_rne_f32.restype = ctypes.c_uint16
-        L.orc_bf16_rne_f64.argtypes = [ctypes.c_double]
-        L.orc_bf16_rne_f64.restype = ctypes.c_uint16
-        L.orc_split_f32.argtypes = [i64, i64, p, i64, p]
-        L.orc_split_f32.restype = u32
-        L.orc_split_f64.argtypes = [i64, i64, p, i64, ctypes.c_int, p, p, p]
-        L.orc_split_f64.restype = u32
-        L.orc_emu_sgemm.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, i64]
-        L.orc_emu_sgemm.restype = u32
-        L.orc_emu_sgemm_entries.argtypes = [i64, i64, i64, p, i64, p, i64, i64, p, p, p, i64]
-        L.orc_emu_sgemm_entries.restype = u32
-        L.orc_emu_dgemm.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, ctypes.c_int,
-                                    ctypes.c_int, i64]
-        L.orc_emu_dgemm.restype = u32
-        L.orc_emu_dgemm_entries.argtypes = [i64, i64, i64, p, i64, p, i64, i64, p, p, p,
-                                            ctypes.c_int, ctypes.c_int, i64]
-        L.orc_emu_dgemm_entries.restype = u32
-        L.orc_ref_gemm_f64.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64]
-        L.orc_ref_gemm_dd.argtypes = [i64, i64, i64, p, i64, p, i64, p, p, i64]
-        L.orc_ref_dd_entries.argtypes = [i64, i64, i64, p, i64, p, i64, i64, p, p, p, p]
-        L.orc_absprod_entries.argtypes = [i64, p, i64, p, i64, i64, p, p, p]
-        L.orc_num_threads.restype = ctypes.c_int
-        L.orc_dot_bf16_f32.argtypes = [i64, p, p]
-        L.orc_dot_bf16_f32.restype = ctypes.c_float
-        _lib = L
+        _lib = _configure(ctypes.CDLL(_LIB))
     return _lib
+
+
+def _configure(L):
+    """Declare the argument and result types of the oracle's C functions."""
+    i64, p, u32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_uint32
+    L.orc_bf16_rne_f32.argtypes = [ctypes.c_float]
+    L.orc_bf16_rne_f32.restype = ctypes.c_uint16
+    L.orc_bf16_rne_f64.argtypes = [ctypes.c_double]
+    L.orc_bf16_rne_f64.restype = ctypes.c_uint16
+    L.orc_split_f32.argtypes = [i64, i64, p, i64, p]
+    L.orc_split_f32.restype = u32
+    L.orc_split_f64.argtypes = [i64, i64, p, i64, ctypes.c_int, p, p, p]
+    L.orc_split_f64.restype = u32
+    L.orc_emu_sgemm.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, i64]
+    L.orc_emu_sgemm.restype = u32
+    L.orc_emu_sgemm_entries.argtypes = [i64, i64, i64, p, i64, p, i64, i64, p, p, p, i64]
+    L.orc_emu_sgemm_entries.restype = u32
+    L.orc_emu_dgemm.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, ctypes.c_int,
+                                ctypes.c_int, i64]
+    L.orc_emu_dgemm.restype = u32
+    L.orc_emu_dgemm_entries.argtypes = [i64, i64, i64, p, i64, p, i64, i64, p, p, p,
+                                        ctypes.c_int, ctypes.c_int, i64]
+    L.orc_emu_dgemm_entries.restype = u32
+    L.orc_ref_gemm_f64.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64]
+    L.orc_ref_gemm_dd.argtypes = [i64, i64, i64, p, i64, p, i64, p, p, i64]
+    L.orc_ref_dd_entries.argtypes = [i64, i64, i64, p, i64, p, i64, i64, p, p, p, p]
+    L.orc_absprod_entries.argtypes = [i64, p, i64, p, i64, i64, p, p, p]
+    L.orc_num_threads.restype = ctypes.c_int
+    L.orc_dot_bf16_f32.argtypes = [i64, p, p]
+    L.orc_dot_bf16_f32.restype = ctypes.c_float
+    return L
 
 
 def _ptr(a: np.ndarray):

@@ -155,6 +155,42 @@ def test_dgemm_definition_bruteforce(nprod, shape):
             assert Fraction(float(C[m, n])) == c, (m, n)
 
 
+def test_dgemm_definition_bruteforce_order_sensitive():
+    """K = 1 and all 21 products: the FP64 chain spans more than 53 bits, so the
+    roundings of the last diagonals depend on the order of the additions
+    (diagonal ascending, i ascending): 4096 entries against exact products
+    added in that order in Python floats (IEEE binary64)."""
+    A = S.make("wide", 43, (64, 1), np.float64)
+    B = S.make("wide", 44, (1, 64), np.float64)
+    C, st = O.emu_dgemm(A, B, 21)
+    assert st == 0
+    sa, _, _, _ = O.split_f64(A)
+    sb, _, _, _ = O.split_f64(B)
+    av = np.vectorize(lambda h: float(bf16_value(h)))(sa[:, :, 0])    # [6, 64]
+    bv = np.vectorize(lambda h: float(bf16_value(h)))(sb[:, 0, :])    # [6, 64]
+    for m in range(64):
+        for n in range(64):
+            c = 0.0
+            for ell in range(6):
+                for i in range(ell + 1):
+                    c = c + av[i, m] * bv[ell - i, n]     # exact product (<= 16 bits)
+            assert C[m, n] == c, (m, n)
+
+
+def test_dot_bf16_f32_ties_to_even():
+    """Exact sums halfway between two binary32 values round to the even one."""
+    one, tiny = 0x3F80, 0x3380                     # BF16 1.0 and 2^-24
+    three_tiny = 0x3440                            # 3 * 2^-24
+    cases = [([one, tiny], 1.0),                   # 1 + 2^-24 -> 1
+             ([one, three_tiny], 1.0 + 2.0 ** -22),   # 1 + 3 2^-24 -> 1 + 2^-22
+             ([0xBF80, 0xB380], -1.0)]             # sign symmetric
+    for xs, want in cases:
+        x = np.array(xs, dtype=np.uint16)
+        y = np.array([one, one], dtype=np.uint16)
+        assert bf16_value(x[1]) in (Fraction(1, 2 ** 24), Fraction(3, 2 ** 24), Fraction(-1, 2 ** 24))
+        assert O.dot_bf16_f32(x, y) == want, (xs, want)
+
+
 def test_dot_bf16_f32_correct_rounding_wide_range():
     rng = np.random.default_rng(9)
     for trial in range(40):

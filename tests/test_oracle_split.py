@@ -46,6 +46,10 @@ def test_bf16_rne_f64_against_fractions(seed):
     vals = np.concatenate([
         rng.standard_normal(300) * 2.0 ** rng.integers(-140, 130, 300),
         [0.0, -0.0, 2.0 ** -133, 2.0 ** -134, 3 * 2.0 ** -135, 2.0 ** -126 * (1 - 2.0 ** -9)],
+        # a detour through binary32 would round these twice: first onto the
+        # BF16 midpoint, then to even; one rounding goes the other way
+        [1 + 2.0 ** -8 + 2.0 ** -30, -(1 + 2.0 ** -8 + 2.0 ** -30), 1 + 3 * 2.0 ** -8 - 2.0 ** -30,
+         (1 + 2.0 ** -8 + 2.0 ** -40) * 2.0 ** 50],
     ])
     for x in vals:
         h = O.bf16_rne_f64(float(x))
