@@ -92,6 +92,9 @@ def main():
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run one plain device-to-device copy of this many MiB: the "
                          "reference kernel that scales rocprofv3 FETCH_SIZE/WRITE_SIZE readings")
+    ap.add_argument("--scope", choices=("operand", "rowcol"), default="operand",
+                    help="FP64 split exponents: the paper's operand-wide chain (default) or the "
+                         "scale-aware row/column weights")
     ap.add_argument("--no-native", action="store_true",
                     help="skip timing the vendor library's native FP32/FP64 GEMM (context)")
     ap.add_argument("--print-source-hash", action="store_true",
@@ -111,6 +114,8 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    scope = emu.SCOPE_ROWCOL if args.scope == "rowcol" else emu.SCOPE_OPERAND
+    emu.set_split_scope(scope)
     if args.copy_calibration_mib > 0:
         nbytes = args.copy_calibration_mib << 20
         src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
@@ -235,7 +240,7 @@ def main():
         bitexact = {}
         for p in (6, 10, 15, 21):
             tc0 = time.perf_counter()
-            orc64, _ = O.emu_dgemm_entries(A64, B64, rows, cols, p)
+            orc64, _ = O.emu_dgemm_entries(A64, B64, rows, cols, p, scope=scope)
             t_total += time.perf_counter() - tc0
             got64 = C64[p][: args.cpu_rows].cpu().numpy().ravel()
             bitexact[str(p)] = bool(np.array_equal(got64, orc64))
@@ -267,6 +272,7 @@ def main():
             "workload": (f"M=N=K={n}: emu-SGEMM (3 comps, 6 products, standard-normal FP32) + "
                          f"emu-DGEMM nprod 6/10/15/21 (six slices, FP64 s*m*2^e, e in [-20,20])"),
             "M": n, "N": n, "K": n, "calls_per_step": len(VARIANTS),
+            "fp64_split_scope": args.scope,
         },
         "per_variant": per_variant,
         "roofline": roofline,

@@ -65,6 +65,21 @@ extern "C" {
 #define EMU_SPLIT_SYM 0
 #define EMU_SPLIT_LITERAL 1
 
+/* Exponent scope of the FP64 split (emu_set_split_scope).
+   OPERAND (default): the paper's split, one exponent chain v^(r) per operand
+   (Eq. fp64split, maxima over the whole operand).
+   ROWCOL: the scale-aware form the paper names as its key future step
+   (Sec. 9), with stored power-of-two weights as in Eq. (ozakiscaled) at row /
+   column granularity: every row m of A is divided by 2^sA_m and every column
+   n of B by 2^sB_n, s = ceil(log2 max|x|) over that row or column (0 if it has
+   no nonzero finite entry); the scaled operands get the operand-wide split;
+   the GEMM multiplies the weights back, C_mn = 2^(sA_m + sB_n) C'_mn.  The
+   scalings are exact (powers of two), so the domain becomes: finite inputs
+   whose nonzero entries lie within 2^-126 of their row's (A) or column's (B)
+   largest magnitude, and results that neither overflow nor underflow FP64. */
+#define EMU_SCOPE_OPERAND 0
+#define EMU_SCOPE_ROWCOL 1
+
 /* Emulated SGEMM, Algorithm fp32 (Sec. 4.2, Eq. fp32split and fp32six):
    each FP32 operand is split into three BF16 components; the six products
    A_iB_j with i + j < 3 are evaluated with FP32 accumulation on bf16 MFMA and
@@ -95,6 +110,12 @@ int emu_set_stream(void *hip_stream);
    EMU_EINVAL for any other value. */
 int emu_set_split_mode(int mode);
 
+/* Exponent scope of the FP64 split for subsequent emu_dgemm and emu_split_f64
+   calls: EMU_SCOPE_OPERAND (default) or EMU_SCOPE_ROWCOL (see above).  In the
+   ROWCOL scope the domain checks behind EMU_STATUS_RANGE apply to the scaled
+   operands.  EMU_EINVAL for any other value. */
+int emu_set_split_scope(int scope);
+
 /* Synchronises the current stream, stores in *flags the EMU_STATUS_* bits
    accumulated by all calls since the previous emu_domain_status, and clears
    them.  EMU_EINVAL if flags is NULL. */
@@ -123,9 +144,20 @@ int emu_split_f32(int64_t R, int64_t Cc, const float *X, int64_t ldx, int as_b, 
    X is R x Cc row-major FP64 (device, ldx); as_b as for emu_split_f32.
    slices (device) receives [6][R][Cc] BF16 bit patterns; v (device, int32[6])
    receives v^(r) = ceil(log2 max|X^(r)|) per level, INT32_MIN for a level
-   whose residual is identically zero. */
+   whose residual is identically zero.  In the ROWCOL scope these are the
+   slices and exponents of the scaled operand (rows of X scaled when as_b = 0,
+   columns when as_b = 1). */
 int emu_split_f64(int64_t R, int64_t Cc, const double *X, int64_t ldx, int as_b,
                   uint16_t *slices, int32_t *v);
+
+/* Test hook: the weights of the ROWCOL scope.  X is R x Cc row-major FP64
+   (device, ldx); s (device, int32) receives ceil(log2 max|x|) over each row
+   (by_col = 0, R entries) or each column (by_col = 1, Cc entries), ignoring
+   non-finite entries, 0 for a row or column without a nonzero finite entry.
+   EMU_EINVAL for negative sizes, ldx < max(1, Cc), by_col not 0 or 1, or a
+   NULL pointer with nonzero extent. */
+int emu_scale_exponents(int64_t R, int64_t Cc, const double *X, int64_t ldx, int by_col,
+                        int32_t *s);
 
 /* Phase timing, the analog of the paper's runtime breakdown (Sec. 8.4):
    decomposition + packing versus the component-product GEMM with its

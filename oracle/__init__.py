@@ -13,7 +13,9 @@ Functions (all operands row-major numpy arrays, all on the host):
 * ``split_f64(X, mode)`` -> (uint16 [6, R, C], v[6], residual A^(6), status)
                                                   Eq. (fp64split), Sec. 4.3
 * ``emu_sgemm(A, B)``    -> FP32 C               Algorithm fp32 + Sec. 6.2/6.3 order
-* ``emu_dgemm(A, B, nprod, mode)`` -> FP64 C     Algorithm fp64, Eq. (fp64reconstruction)
+* ``emu_dgemm(A, B, nprod, mode, scope)`` -> FP64 C   Algorithm fp64, Eq. (fp64reconstruction)
+* ``scale_exponents(X, by_col)`` -> per-row / per-column power-of-two weights of
+                                    the scale-aware split (Eq. ozakiscaled, Sec. 9)
 * ``*_entries``          -> the same for selected (row, col) entries
 * ``ref_gemm_f64``, ``ref_gemm_dd``, ``ref_dd_entries`` -> references
 * ``e_F``, ``e_scaled``  -> Eq. (froerror) and Eq. (scalederror), Sec. 7.3
@@ -33,6 +35,14 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 
 SPLIT_SYM = 0
 SPLIT_LITERAL = 1
+# Exponent scope of the FP64 split: the paper's operand-wide maxima (default),
+# or the scale-aware form named as future work in Sec. 9: every row of A and
+# every column of B is first divided by a stored power-of-two weight 2^s with
+# s = ceil(log2 max|row|) (the per-row form of the weights 2^v of
+# Eq. ozakiscaled), split operand-wide, and the weights are multiplied back
+# into the FP64 result, C_mn = 2^(sA_m + sB_n) C'_mn.
+SCOPE_OPERAND = 0
+SCOPE_ROWCOL = 1
 KC = 256  # reduction-panel length B_K of the paper's blocked loop (Sec. 6.1)
 
 ST_NAN, ST_RANGE, ST_SUBNORMAL, ST_OVERFLOW, ST_INEXACT32 = 1, 2, 4, 8, 16
@@ -193,7 +203,30 @@ def emu_sgemm_entries(A, B, rows, cols, kc: int = KC):
     return out, int(st)
 
 
-def emu_dgemm(A: np.ndarray, B: np.ndarray, nprod: int, mode: int = SPLIT_SYM, kc: int = KC):
+def scale_exponents(X: np.ndarray, by_col: bool = False) -> np.ndarray:
+    """ceil(log2 max|x|) over each row (or column) of X, from the exact
+    frexp decomposition; 0 for a row without nonzero finite entries."""
+    X = np.asarray(X, dtype=np.float64)
+    a = np.where(np.isfinite(X), np.abs(X), 0.0)
+    m = a.max(axis=0 if by_col else 1) if X.size else np.zeros(X.shape[1 if by_col else 0])
+    f, e = np.frexp(m)
+    s = np.where(f == 0.5, e - 1, e)
+    return np.where(m > 0, s, 0).astype(np.int32)
+
+
+def scaled_operands(A: np.ndarray, B: np.ndarray):
+    """(sA, sB, A 2^-sA by rows, B 2^-sB by columns): exact power-of-two scalings."""
+    sA = scale_exponents(A, by_col=False)
+    sB = scale_exponents(B, by_col=True)
+    return sA, sB, np.ldexp(A, -sA[:, None]), np.ldexp(B, -sB[None, :])
+
+
+def emu_dgemm(A: np.ndarray, B: np.ndarray, nprod: int, mode: int = SPLIT_SYM, kc: int = KC,
+              scope: int = SCOPE_OPERAND):
+    if scope == SCOPE_ROWCOL:
+        sA, sB, As, Bs = scaled_operands(_c(A, np.float64), _c(B, np.float64))
+        C, st = emu_dgemm(As, Bs, nprod, mode, kc)
+        return np.ldexp(C, sA[:, None] + sB[None, :]), st
     A, B = _c(A, np.float64), _c(B, np.float64)
     M, K = A.shape
     K2, N = B.shape
@@ -204,7 +237,13 @@ def emu_dgemm(A: np.ndarray, B: np.ndarray, nprod: int, mode: int = SPLIT_SYM, k
     return C, int(st)
 
 
-def emu_dgemm_entries(A, B, rows, cols, nprod: int, mode: int = SPLIT_SYM, kc: int = KC):
+def emu_dgemm_entries(A, B, rows, cols, nprod: int, mode: int = SPLIT_SYM, kc: int = KC,
+                      scope: int = SCOPE_OPERAND):
+    if scope == SCOPE_ROWCOL:
+        sA, sB, As, Bs = scaled_operands(_c(A, np.float64), _c(B, np.float64))
+        r, c = _idx(rows, cols)
+        out, st = emu_dgemm_entries(As, Bs, r, c, nprod, mode, kc)
+        return np.ldexp(out, sA[r] + sB[c]), st
     A, B = _c(A, np.float64), _c(B, np.float64)
     M, K = A.shape
     N = B.shape[1]

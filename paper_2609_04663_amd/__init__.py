@@ -11,6 +11,8 @@ library is not built, importing the functions raises.
     dgemm(A, B, nprod, C=None)     -> C = A @ B, FP64, six slices / nprod products
     split_f32(X, as_b=False)       -> int16 tensor [3, R, C] of BF16 bit patterns
     split_f64(X, as_b=False)       -> (int16 tensor [6, R, C], int32 tensor [6])
+    set_split_scope(scope)         -> SCOPE_OPERAND (default) or SCOPE_ROWCOL weights
+    scale_exponents(X, by_col)     -> int32 tensor of the ROWCOL weights
     domain_status()                -> EMU_STATUS_* bits accumulated since last call
 """
 from __future__ import annotations
@@ -26,12 +28,13 @@ LIB_PATH = os.path.join(_HERE, "libemu.so")
 EMU_OK, EMU_EINVAL, EMU_EHIP, EMU_ENOMEM = 0, 1, 2, 3
 STATUS_NAN, STATUS_RANGE, STATUS_SUBNORMAL, STATUS_OVERFLOW = 1, 2, 4, 8
 SPLIT_SYM, SPLIT_LITERAL = 0, 1
+SCOPE_OPERAND, SCOPE_ROWCOL = 0, 1
 NPROD = (6, 10, 15, 21)
 
 EXPORTS = ("emu_sgemm", "emu_dgemm", "emu_set_stream", "emu_set_split_mode",
            "emu_domain_status", "emu_last_error", "emu_release_workspace",
            "emu_workspace_bytes", "emu_split_f32", "emu_split_f64", "emu_profile_enable",
-           "emu_profile_read")
+           "emu_profile_read", "emu_set_split_scope", "emu_scale_exponents")
 
 
 class EmuError(RuntimeError):
@@ -56,6 +59,8 @@ def lib() -> ctypes.CDLL:
         L.emu_dgemm.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, ci]
         L.emu_set_stream.argtypes = [p]
         L.emu_set_split_mode.argtypes = [ci]
+        L.emu_set_split_scope.argtypes = [ci]
+        L.emu_scale_exponents.argtypes = [i64, i64, p, i64, ci, p]
         L.emu_domain_status.argtypes = [ctypes.POINTER(ctypes.c_uint)]
         L.emu_last_error.restype = ctypes.c_char_p
         L.emu_workspace_bytes.restype = i64
@@ -65,7 +70,8 @@ def lib() -> ctypes.CDLL:
         L.emu_profile_read.argtypes = [i64, p, p, ctypes.POINTER(ctypes.c_int64)]
         for name in ("emu_sgemm", "emu_dgemm", "emu_set_stream", "emu_set_split_mode",
                      "emu_domain_status", "emu_release_workspace", "emu_split_f32",
-                     "emu_split_f64", "emu_profile_enable", "emu_profile_read"):
+                     "emu_split_f64", "emu_profile_enable", "emu_profile_read",
+                     "emu_set_split_scope", "emu_scale_exponents"):
             getattr(L, name).restype = ci
         _lib = L
     return _lib
@@ -149,6 +155,20 @@ def split_f64(X: torch.Tensor, as_b: bool = False):
 
 def set_split_mode(mode: int):
     _check(lib().emu_set_split_mode(int(mode)))
+
+
+def set_split_scope(scope: int):
+    """SCOPE_OPERAND (the paper's split) or SCOPE_ROWCOL (row/column weights)."""
+    _check(lib().emu_set_split_scope(int(scope)))
+
+
+def scale_exponents(X: torch.Tensor, by_col: bool = False) -> torch.Tensor:
+    _mat(X, torch.float64, "X")
+    R, Cc = X.shape
+    out = torch.empty(Cc if by_col else R, dtype=torch.int32, device=X.device)
+    _bind_stream(X.device)
+    _check(lib().emu_scale_exponents(R, Cc, X.data_ptr(), _ld(X), int(by_col), out.data_ptr()))
+    return out
 
 
 def domain_status() -> int:

@@ -18,6 +18,7 @@ using namespace emu;
 
 hipStream_t g_stream = nullptr;
 int g_split_mode = EMU_SPLIT_SYM;
+int g_split_scope = EMU_SCOPE_OPERAND;
 std::string g_err;
 
 // Workspace: [status word (offset 0), two FP64 split states (offset 128): 512 B]
@@ -108,6 +109,22 @@ unsigned *ws_status() { return reinterpret_cast<unsigned *>(g_ws.base); }
 F64SplitState *ws_states() { return reinterpret_cast<F64SplitState *>(g_ws.base + 128); }
 uint16_t *ws_planes(size_t off) { return reinterpret_cast<uint16_t *>(g_ws.base + HDR + off); }
 
+// Scale-aware split scratch after the planes (256-byte aligned): 64-bit maxima
+// for the nA rows of A and the nB columns of B, then their int32 exponents.
+struct ScaleArea {
+    unsigned long long *mb;   // [nA + nB]
+    int *sa, *sb;             // [nA], [nB]
+};
+size_t scale_bytes(int64_t nA, int64_t nB) { return 256 + (size_t)(nA + nB) * 12; }
+ScaleArea ws_scales(size_t planes_bytes, int64_t nA, int64_t nB) {
+    const size_t off = (HDR + planes_bytes + 255) / 256 * 256;
+    ScaleArea a;
+    a.mb = reinterpret_cast<unsigned long long *>(g_ws.base + off);
+    a.sa = reinterpret_cast<int *>(a.mb + nA + nB);
+    a.sb = a.sa + nA;
+    return a;
+}
+
 int nprod_to_d(int nprod) {
     switch (nprod) {
         case 6: return 3;
@@ -162,6 +179,13 @@ int emu_set_split_mode(int mode) {
     if (mode != EMU_SPLIT_SYM && mode != EMU_SPLIT_LITERAL)
         return fail(EMU_EINVAL, "split mode must be EMU_SPLIT_SYM or EMU_SPLIT_LITERAL");
     g_split_mode = mode;
+    return EMU_OK;
+}
+
+int emu_set_split_scope(int scope) {
+    if (scope != EMU_SCOPE_OPERAND && scope != EMU_SCOPE_ROWCOL)
+        return fail(EMU_EINVAL, "split scope must be EMU_SCOPE_OPERAND or EMU_SCOPE_ROWCOL");
+    g_split_scope = scope;
     return EMU_OK;
 }
 
@@ -276,19 +300,30 @@ int emu_dgemm(int64_t M, int64_t N, int64_t K, const double *A, int64_t lda, con
     // Only the d slices the retained products read are materialised; the
     // levels after them never influence slices 0 .. d-1.
     const Shape s = plan(M, N, K, d, dgemm_mt(d), DGEMM_NT);
-    rc = ensure_workspace(s.bytesA + s.bytesB);
+    const bool scaled = g_split_scope == EMU_SCOPE_ROWCOL;
+    rc = ensure_workspace(s.bytesA + s.bytesB + (scaled ? scale_bytes(M, N) : 0));
     if (rc) return rc;
     uint16_t *Ap = ws_planes(0), *Bp = ws_planes(s.bytesA);
     F64SplitState *st = ws_states();
+    const ScaleArea sc = ws_scales(s.bytesA + s.bytesB, M, N);
     prof_mark(0);
-    hipError_t e = launch_split_f64(A, M, K, lda, false, Ap, s.KB, s.RpadA, d, g_split_mode, st,
-                                    ws_status(), g_stream);
+    hipError_t e = hipSuccess;
+    if (scaled) {
+        // weights: rows of A, columns of B (the scale-aware split)
+        e = launch_scale_exponents(A, M, K, lda, false, sc.mb, sc.sa, g_stream);
+        if (e != hipSuccess) return hip_fail(e, "scale_exponents(A)");
+        e = launch_scale_exponents(B, K, N, ldb, true, sc.mb + M, sc.sb, g_stream);
+        if (e != hipSuccess) return hip_fail(e, "scale_exponents(B)");
+    }
+    e = launch_split_f64(A, M, K, lda, false, scaled ? sc.sa : nullptr, Ap, s.KB, s.RpadA, d,
+                         g_split_mode, st, ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f64(A)");
-    e = launch_split_f64(B, K, N, ldb, true, Bp, s.KB, s.RpadB, d, g_split_mode, st + 1,
-                         ws_status(), g_stream);
+    e = launch_split_f64(B, K, N, ldb, true, scaled ? sc.sb : nullptr, Bp, s.KB, s.RpadB, d,
+                         g_split_mode, st + 1, ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f64(B)");
     prof_mark(1);
-    e = launch_gemm_f64(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, d, g_stream);
+    e = launch_gemm_f64(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, scaled ? sc.sa : nullptr,
+                        scaled ? sc.sb : nullptr, d, g_stream);
     if (e != hipSuccess) return hip_fail(e, "gemm_f64");
     prof_mark(2);
     return EMU_OK;
@@ -329,12 +364,19 @@ int emu_split_f64(int64_t R, int64_t Cc, const double *X, int64_t ldx, int as_b,
     g_err.clear();
     const int64_t rows = as_b ? Cc : R, K = as_b ? R : Cc;
     const Shape s = plan(rows, 1, K, 6, ROW_GROUP, ROW_GROUP);
-    rc = ensure_workspace(s.bytesA > 0 ? s.bytesA : 1);
+    const bool scaled = g_split_scope == EMU_SCOPE_ROWCOL;
+    rc = ensure_workspace((s.bytesA > 0 ? s.bytesA : 1) + (scaled ? scale_bytes(rows, 0) : 0));
     if (rc) return rc;
     uint16_t *P = ws_planes(0);
     F64SplitState *st = ws_states();
-    hipError_t e = launch_split_f64(X, R, Cc, ldx, as_b != 0, P, s.KB, s.RpadA, 6, g_split_mode, st,
-                                    ws_status(), g_stream);
+    const ScaleArea sc = ws_scales(s.bytesA > 0 ? s.bytesA : 1, rows, 0);
+    hipError_t e = hipSuccess;
+    if (scaled) {
+        e = launch_scale_exponents(X, R, Cc, ldx, as_b != 0, sc.mb, sc.sa, g_stream);
+        if (e != hipSuccess) return hip_fail(e, "scale_exponents");
+    }
+    e = launch_split_f64(X, R, Cc, ldx, as_b != 0, scaled ? sc.sa : nullptr, P, s.KB, s.RpadA, 6,
+                         g_split_mode, st, ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f64");
     if (R > 0 && Cc > 0) {
         e = launch_unpack(P, 6, s.KB, s.RpadA, R, Cc, as_b != 0, slices, g_stream);
@@ -343,6 +385,27 @@ int emu_split_f64(int64_t R, int64_t Cc, const double *X, int64_t ldx, int as_b,
     e = launch_copy_v(st, v, g_stream);
     if (e != hipSuccess) return hip_fail(e, "copy_v");
     return EMU_OK;
+}
+
+int emu_scale_exponents(int64_t R, int64_t Cc, const double *X, int64_t ldx, int by_col,
+                        int32_t *s) {
+    if (R < 0 || Cc < 0) return fail(EMU_EINVAL, "R and Cc must be non-negative");
+    if (ldx < (Cc > 1 ? Cc : 1)) return fail(EMU_EINVAL, "ldx < max(1, Cc)");
+    if (by_col != 0 && by_col != 1) return fail(EMU_EINVAL, "by_col must be 0 or 1");
+    const int64_t n = by_col ? Cc : R;
+    if (n > 0 && (!s || (R > 0 && Cc > 0 && !X))) return fail(EMU_EINVAL, "NULL pointer");
+    g_err.clear();
+    if (n == 0) return EMU_OK;
+    int rc = ensure_workspace(scale_bytes(n, 0));
+    if (rc) return rc;
+    const ScaleArea sc = ws_scales(0, n, 0);
+    hipError_t e;
+    if (R == 0 || Cc == 0) {
+        e = launch_fill_f32(reinterpret_cast<float *>(s), 1, n, n, g_stream);   // no entries: 0
+    } else {
+        e = launch_scale_exponents(X, R, Cc, ldx, by_col != 0, sc.mb, s, g_stream);
+    }
+    return e == hipSuccess ? EMU_OK : hip_fail(e, "scale_exponents");
 }
 
 }  // extern "C"

@@ -72,15 +72,22 @@ hipError_t launch_fill_f64(double *C, int64_t M, int64_t N, int64_t ldc, hipStre
 hipError_t launch_split_f32(const float *X, int64_t rows, int64_t cols, int64_t ldx, bool as_b,
                             uint16_t *P, int64_t KB, int64_t Rpad, unsigned *status,
                             hipStream_t s);
+// sc: per-packed-row weights 2^-sc of the scale-aware split, or null
 hipError_t launch_split_f64(const double *X, int64_t rows, int64_t cols, int64_t ldx, bool as_b,
-                            uint16_t *P, int64_t KB, int64_t Rpad, int nlev, int mode,
-                            F64SplitState *st, unsigned *status, hipStream_t s);
+                            const int *sc, uint16_t *P, int64_t KB, int64_t Rpad, int nlev,
+                            int mode, F64SplitState *st, unsigned *status, hipStream_t s);
+// per-row (by_col = 0) or per-column exponents ceil(log2 max|x|) of X; mb is
+// scratch of rows (or cols) 64-bit words
+hipError_t launch_scale_exponents(const double *X, int64_t rows, int64_t cols, int64_t ldx,
+                                  bool by_col, unsigned long long *mb, int *sexp, hipStream_t s);
 hipError_t launch_unpack(const uint16_t *P, int nc, int64_t KB, int64_t Rpad, int64_t rows,
                          int64_t cols, bool as_b, uint16_t *out, hipStream_t s);
 hipError_t launch_copy_v(const F64SplitState *st, int32_t *v, hipStream_t s);
 hipError_t launch_gemm_f32(const uint16_t *Ap, const uint16_t *Bp, float *C, int64_t M, int64_t N,
                            int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc, hipStream_t s);
+// sa, sb: row weights of A and column weights of B to restore (C_mn times
+// 2^(sa_m + sb_n)), or both null
 hipError_t launch_gemm_f64(const uint16_t *Ap, const uint16_t *Bp, double *C, int64_t M,
                            int64_t N, int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc,
-                           int d, hipStream_t s);
+                           const int *sa, const int *sb, int d, hipStream_t s);
 }  // namespace emu

@@ -184,9 +184,12 @@ __global__ void f64_state_verify(F64SplitState *st, int nst) {
 
 // max |x| over an operand (level-0 maximum) and the input-domain checks of
 // Eq. (bf16rangefp64).  Rows are strided over blocks, columns over threads.
+// With weights (sc non-null) the operand is read as x 2^-sc[p], p the packed
+// row of x (X's row, or X's column when by_col), and the checks apply to it.
 __global__ __launch_bounds__(SPLIT_THREADS) void f64_maxabs_kernel(
     const double *__restrict__ X, int64_t rows, int64_t cols, int64_t ldx,
-    F64SplitState *__restrict__ st, unsigned *__restrict__ status) {
+    const int *__restrict__ sc, int by_col, F64SplitState *__restrict__ st,
+    unsigned *__restrict__ status) {
     __shared__ unsigned long long red[SPLIT_THREADS / 64];
     double m = 0.0;
     unsigned flags = 0;
@@ -194,7 +197,8 @@ __global__ __launch_bounds__(SPLIT_THREADS) void f64_maxabs_kernel(
     for (int64_t r = blockIdx.x; r < rows; r += gridDim.x) {
         const double *row = X + r * ldx;
         for (int64_t c = threadIdx.x; c < cols; c += SPLIT_THREADS) {
-            const double x = row[c];
+            double x = row[c];
+            if (sc) x = ldexp(x, -sc[by_col ? c : r]);
             const double a = fabs(x);
             if (!__builtin_isfinite(x)) { flags |= ST_NAN; continue; }
             if (x != 0.0 && (a < lo || a > hi)) flags |= ST_RANGE;
@@ -225,9 +229,9 @@ __global__ __launch_bounds__(SPLIT_THREADS) void f64_maxabs_kernel(
 // slices >= d, and they do not influence slices < d).
 template <bool AS_B>
 __global__ __launch_bounds__(SPLIT_THREADS) void split_f64_kernel(
-    const double *__restrict__ X, int64_t rows, int64_t cols, int64_t ldx, u16 *__restrict__ P,
-    int64_t KB, int64_t Rpad, F64SplitState *__restrict__ stp, unsigned *__restrict__ status,
-    int first_pass) {
+    const double *__restrict__ X, int64_t rows, int64_t cols, int64_t ldx,
+    const int *__restrict__ sc, u16 *__restrict__ P, int64_t KB, int64_t Rpad,
+    F64SplitState *__restrict__ stp, unsigned *__restrict__ status, int first_pass) {
     __shared__ unsigned long long red[6][SPLIT_THREADS / 64];
     const int r0 = first_pass ? 0 : stp->replay_from;
     if (r0 < 0) return;                                   // verified: nothing to redo
@@ -250,10 +254,12 @@ __global__ __launch_bounds__(SPLIT_THREADS) void split_f64_kernel(
         const ItemCoords ic = item_coords(pair, RG);
         const int64_t k0 = ic.kb * KBLK + ic.q * 8;
         double x[8];
+        const int wexp = (sc && ic.prow < prow_lim) ? -sc[ic.prow] : 0;   // row weight 2^-s
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const bool ok = ic.prow < prow_lim && k0 + i < k_lim;
             x[i] = ok ? (AS_B ? X[(k0 + i) * ldx + ic.prow] : X[ic.prow * ldx + k0 + i]) : 0.0;
+            if (sc) x[i] = ldexp(x[i], wexp);
         }
         u16x8 out[6];
 #pragma unroll
@@ -302,6 +308,76 @@ __global__ __launch_bounds__(SPLIT_THREADS) void split_f64_kernel(
             if (b) atomicMax(&stp->maxbits[r], b);
         }
     }
+}
+
+// ---------------------------------------------------------------------------
+// Weights of the scale-aware split: s_p = ceil(log2 max|x|) over each row of X
+// (by_col = 0) or each column (by_col = 1), non-finite entries ignored, 0 for
+// a row without nonzero entries.  The maxima are reduced as bit patterns of
+// non-negative doubles (whose unsigned order is the numeric order).
+
+// one block per row, threads across the row
+__global__ __launch_bounds__(SPLIT_THREADS) void row_maxbits_kernel(
+    const double *__restrict__ X, int64_t rows, int64_t cols, int64_t ldx,
+    unsigned long long *__restrict__ mb) {
+    __shared__ unsigned long long red[SPLIT_THREADS / 64];
+    for (int64_t r = blockIdx.x; r < rows; r += gridDim.x) {
+        double m = 0.0;
+        for (int64_t c = threadIdx.x; c < cols; c += SPLIT_THREADS) {
+            const double x = X[r * ldx + c];
+            if (__builtin_isfinite(x)) m = fmax(m, fabs(x));
+        }
+        for (int off = 32; off > 0; off >>= 1) m = fmax(m, __shfl_xor(m, off));
+        if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = dbits(m);
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            unsigned long long b = red[0];
+            for (int i = 1; i < SPLIT_THREADS / 64; ++i) b = red[i] > b ? red[i] : b;
+            mb[r] = b;
+        }
+        __syncthreads();
+    }
+}
+
+// 64 columns per block and a slice of the rows per blockIdx.y; lanes run
+// along the columns (coalesced), the four waves over rows; one atomic maximum
+// per column and block.  mb must be zero on entry.
+__global__ __launch_bounds__(SPLIT_THREADS) void col_maxbits_kernel(
+    const double *__restrict__ X, int64_t rows, int64_t cols, int64_t ldx,
+    unsigned long long *__restrict__ mb) {
+    __shared__ unsigned long long red[SPLIT_THREADS / 64][64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int64_t c = (int64_t)blockIdx.x * 64 + lane;
+    const int64_t per = (rows + gridDim.y - 1) / gridDim.y;
+    const int64_t r0 = (int64_t)blockIdx.y * per, r1 = r0 + per < rows ? r0 + per : rows;
+    double m = 0.0;
+    if (c < cols)
+        for (int64_t r = r0 + w; r < r1; r += SPLIT_THREADS / 64) {
+            const double x = X[r * ldx + c];
+            if (__builtin_isfinite(x)) m = fmax(m, fabs(x));
+        }
+    red[w][lane] = dbits(m);
+    __syncthreads();
+    if (w == 0 && c < cols) {
+        unsigned long long b = red[0][lane];
+        for (int i = 1; i < SPLIT_THREADS / 64; ++i) b = red[i][lane] > b ? red[i][lane] : b;
+        if (b) atomicMax(&mb[c], b);
+    }
+}
+
+__global__ void maxbits_to_exponent_kernel(const unsigned long long *__restrict__ mb, int64_t n,
+                                           int *__restrict__ s) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const double m = __longlong_as_double((long long)mb[i]);
+        s[i] = (m > 0.0) ? ceil_log2_pos(m) : 0;
+    }
+}
+
+__global__ void fill_u64_kernel(unsigned long long *p, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = 0ull;
 }
 
 // Test hook: packed planes back to plain row-major planes in X's orientation.
@@ -364,23 +440,44 @@ hipError_t launch_split_f32(const float *X, int64_t rows, int64_t cols, int64_t 
 // then verify/replay until every level is verified (at most nlev - 1 replays,
 // each a no-op once the chain is verified), then a final verify.
 hipError_t launch_split_f64(const double *X, int64_t rows, int64_t cols, int64_t ldx, bool as_b,
-                            uint16_t *P, int64_t KB, int64_t Rpad, int nlev, int mode,
-                            F64SplitState *st, unsigned *status, hipStream_t s) {
+                            const int *sc, uint16_t *P, int64_t KB, int64_t Rpad, int nlev,
+                            int mode, F64SplitState *st, unsigned *status, hipStream_t s) {
     f64_state_init<<<1, 64, 0, s>>>(st, 1, nlev, mode);
     const int gm = (int)(rows < 2048 ? (rows > 0 ? rows : 1) : 2048);
-    f64_maxabs_kernel<<<gm, SPLIT_THREADS, 0, s>>>(X, rows, cols, ldx, st, status);
+    f64_maxabs_kernel<<<gm, SPLIT_THREADS, 0, s>>>(X, rows, cols, ldx, sc, as_b ? 1 : 0, st, status);
     f64_state_speculate<<<1, 64, 0, s>>>(st, 1);
     const int g = grid_for_pairs(KB * (Rpad / ROWS_PER_BLOCK));
     for (int pass = 0; pass < nlev; ++pass) {
         if (pass > 0) f64_state_verify<<<1, 64, 0, s>>>(st, 1);
         if (as_b)
-            split_f64_kernel<true><<<g, SPLIT_THREADS, 0, s>>>(X, rows, cols, ldx, P, KB, Rpad, st,
-                                                                status, pass == 0);
+            split_f64_kernel<true><<<g, SPLIT_THREADS, 0, s>>>(X, rows, cols, ldx, sc, P, KB, Rpad,
+                                                                st, status, pass == 0);
         else
-            split_f64_kernel<false><<<g, SPLIT_THREADS, 0, s>>>(X, rows, cols, ldx, P, KB, Rpad, st,
-                                                                 status, pass == 0);
+            split_f64_kernel<false><<<g, SPLIT_THREADS, 0, s>>>(X, rows, cols, ldx, sc, P, KB, Rpad,
+                                                                 st, status, pass == 0);
     }
     f64_state_verify<<<1, 64, 0, s>>>(st, 1);
+    return hipGetLastError();
+}
+
+hipError_t launch_scale_exponents(const double *X, int64_t rows, int64_t cols, int64_t ldx,
+                                  bool by_col, unsigned long long *mb, int *sexp, hipStream_t s) {
+    const int64_t n = by_col ? cols : rows;
+    if (n == 0) return hipSuccess;
+    const int fg = (int)((n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024);
+    if (by_col) {
+        fill_u64_kernel<<<fg, 256, 0, s>>>(mb, n);
+        const int64_t gx = (cols + 63) / 64;
+        int64_t gy = (rows + 255) / 256;                  // about 256 rows per block
+        if (gy > 65535) gy = 65535;
+        if (gx * gy > 16384) gy = 16384 / gx > 1 ? 16384 / gx : 1;
+        col_maxbits_kernel<<<dim3((unsigned)gx, (unsigned)gy), SPLIT_THREADS, 0, s>>>(X, rows, cols,
+                                                                                      ldx, mb);
+    } else {
+        const int g = (int)(rows < 8192 ? rows : 8192);
+        row_maxbits_kernel<<<g, SPLIT_THREADS, 0, s>>>(X, rows, cols, ldx, mb);
+    }
+    maxbits_to_exponent_kernel<<<fg, 256, 0, s>>>(mb, n, sexp);
     return hipGetLastError();
 }
 

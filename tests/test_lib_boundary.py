@@ -89,3 +89,17 @@ def test_split_mode_and_status_arguments(L):
     assert L.emu_set_split_mode(emu.SPLIT_SYM) == emu.EMU_OK
     assert L.emu_domain_status(None) == emu.EMU_EINVAL
     assert L.emu_set_stream(None) == emu.EMU_OK
+
+
+def test_split_scope_and_scale_hook_arguments(L):
+    import paper_2609_04663_amd as emu
+    assert L.emu_set_split_scope(2) == emu.EMU_EINVAL
+    assert L.emu_set_split_scope(-1) == emu.EMU_EINVAL
+    assert L.emu_set_split_scope(emu.SCOPE_ROWCOL) == emu.EMU_OK
+    assert L.emu_set_split_scope(emu.SCOPE_OPERAND) == emu.EMU_OK
+    assert L.emu_scale_exponents(-1, 4, P, 4, 0, P) == emu.EMU_EINVAL      # negative R
+    assert L.emu_scale_exponents(4, 4, P, 3, 0, P) == emu.EMU_EINVAL       # ldx < Cc
+    assert L.emu_scale_exponents(4, 4, P, 4, 2, P) == emu.EMU_EINVAL       # by_col
+    assert L.emu_scale_exponents(4, 4, None, 4, 0, P) == emu.EMU_EINVAL    # NULL X
+    assert L.emu_scale_exponents(4, 4, P, 4, 1, None) == emu.EMU_EINVAL    # NULL s
+    assert L.emu_scale_exponents(0, 4, None, 4, 0, None) == emu.EMU_OK     # nothing to do
