@@ -178,7 +178,9 @@ def main():
         log("bench: native FP32/FP64 GEMM (vendor library) for context")
         native = {"fp32_tflops": round(lib_rate(dA32, dB32, 3), 2),
                   "fp64_tflops": round(lib_rate(dA64, dB64, 2), 2),
-                  "library": "torch.matmul (hipBLASLt/rocBLAS), same inputs"}
+                  # the headroom of the method: one plain BF16 GEMM (FP32 accumulation)
+                  "bf16_tflops": round(lib_rate(dA32.to(torch.bfloat16), dB32.to(torch.bfloat16), 5), 2),
+                  "library": "torch.matmul (hipBLASLt/rocBLAS), same inputs (bf16: RNE-cast)"}
 
     flop = 2.0 * n ** 3
     elapsed = t1 - t0
@@ -203,6 +205,7 @@ def main():
     if native:
         native["emu_sgemm_speedup_vs_native_fp32"] = round(
             per_variant["emu-SGEMM"]["effective_tflops"] / native["fp32_tflops"], 3)
+        native["bf16_frac_of_peak"] = round(native["bf16_tflops"] / PEAK_BF16_TFLOPS, 4)
         native["emu_dgemm_speedup_vs_native_fp64"] = {
             str(p): round(per_variant[f"emu-DGEMM-{p}"]["effective_tflops"] / native["fp64_tflops"], 3)
             for p in (6, 10, 15, 21)}
