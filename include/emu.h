@@ -101,6 +101,27 @@ int emu_sgemm(int64_t M, int64_t N, int64_t K, const float *A, int64_t lda, cons
 int emu_dgemm(int64_t M, int64_t N, int64_t K, const double *A, int64_t lda, const double *B,
               int64_t ldb, double *C, int64_t ldc, int nprod);
 
+/* BLAS forms (the "more complete BLAS semantics" of Sec. 9):
+     C = alpha op(A) op(B) + beta C,  row-major, op(X) = X or X^T.
+   transa, transb: 'N' (op(X) = X) or 'T' ('C' is accepted as 'T'; lower case
+   too).  op(A) is M x K: A is M x K with lda >= max(1, K) for 'N', K x M with
+   lda >= max(1, M) for 'T'.  op(B) is K x N: B is K x N with ldb >= max(1, N)
+   for 'N', N x K with ldb >= max(1, K) for 'T'.  With P the emulated product
+   (the value emu_sgemm / emu_dgemm give for op(A) op(B)), each entry becomes
+   fl(alpha P) if beta == 0 -- C is then not read and may hold anything -- and
+   fl(fl(alpha P) + fl(beta C)) otherwise (no fused multiply-add), so
+   alpha = 1, beta = 0 is emu_sgemm / emu_dgemm exactly.  alpha == 0 or K == 0:
+   A and B are not read and C = beta C (0 when beta == 0).  Transposed operands
+   are packed from their stored layout directly, so op(A) op(B) gives the same
+   bits as the plain call on explicitly transposed copies.  Errors as for
+   emu_sgemm / emu_dgemm, plus EMU_EINVAL for another transa / transb. */
+int emu_sgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, float alpha,
+                 const float *A, int64_t lda, const float *B, int64_t ldb, float beta, float *C,
+                 int64_t ldc);
+int emu_dgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, double alpha,
+                 const double *A, int64_t lda, const double *B, int64_t ldb, double beta,
+                 double *C, int64_t ldc, int nprod);
+
 /* Stream for subsequent calls (a hipStream_t); NULL selects the default
    stream.  Always returns EMU_OK. */
 int emu_set_stream(void *hip_stream);

@@ -254,6 +254,45 @@ def emu_dgemm_entries(A, B, rows, cols, nprod: int, mode: int = SPLIT_SYM, kc: i
     return out, int(st)
 
 
+def _blas_out(P, C, alpha, beta, dtype):
+    """fl(alpha P) when beta == 0 (C unread), else fl(fl(alpha P) + fl(beta C)),
+    in the output precision, elementwise (numpy rounds every operation)."""
+    a, b = dtype(alpha), dtype(beta)
+    if b == 0:
+        return (a * P).astype(dtype)
+    return (a * P + b * np.asarray(C, dtype=dtype)).astype(dtype)
+
+
+def _scale_only(C, beta, shape, dtype):
+    """The alpha == 0 or K == 0 result: beta C, or 0 when beta == 0 (C unread)."""
+    b = dtype(beta)
+    return np.zeros(shape, dtype) if b == 0 else (b * np.asarray(C, dtype=dtype)).astype(dtype)
+
+
+def _op(X, trans):
+    return np.ascontiguousarray(X.T) if trans in ("T", "t", "C", "c") else X
+
+
+def emu_sgemm_ex(A, B, C=None, transa="N", transb="N", alpha=1.0, beta=0.0, kc: int = KC):
+    """The BLAS form alpha op(A) op(B) + beta C (row-major, A and B as stored)."""
+    opA, opB = _op(_c(A, np.float32), transa), _op(_c(B, np.float32), transb)
+    M, N = opA.shape[0], opB.shape[1]
+    if alpha == 0 or opA.shape[1] == 0:
+        return _scale_only(C, beta, (M, N), np.float32), 0
+    P, st = emu_sgemm(opA, opB, kc)
+    return _blas_out(P, C, alpha, beta, np.float32), st
+
+
+def emu_dgemm_ex(A, B, nprod: int, C=None, transa="N", transb="N", alpha=1.0, beta=0.0,
+                 mode: int = SPLIT_SYM, kc: int = KC, scope: int = SCOPE_OPERAND):
+    opA, opB = _op(_c(A, np.float64), transa), _op(_c(B, np.float64), transb)
+    M, N = opA.shape[0], opB.shape[1]
+    if alpha == 0 or opA.shape[1] == 0:
+        return _scale_only(C, beta, (M, N), np.float64), 0
+    P, st = emu_dgemm(opA, opB, nprod, mode, kc, scope)
+    return _blas_out(P, C, alpha, beta, np.float64), st
+
+
 def ref_gemm_f64(A, B):
     A = np.ascontiguousarray(np.asarray(A, dtype=np.float64))
     B = np.ascontiguousarray(np.asarray(B, dtype=np.float64))

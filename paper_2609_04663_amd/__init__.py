@@ -9,6 +9,7 @@ library is not built, importing the functions raises.
 
     sgemm(A, B, C=None)            -> C = A @ B, FP32, 3 components / 6 products
     dgemm(A, B, nprod, C=None)     -> C = A @ B, FP64, six slices / nprod products
+    sgemm_ex / dgemm_ex(..., transa, transb, alpha, beta) -> BLAS form alpha op(A) op(B) + beta C
     split_f32(X, as_b=False)       -> int16 tensor [3, R, C] of BF16 bit patterns
     split_f64(X, as_b=False)       -> (int16 tensor [6, R, C], int32 tensor [6])
     set_split_scope(scope)         -> SCOPE_OPERAND (default) or SCOPE_ROWCOL weights
@@ -34,7 +35,8 @@ NPROD = (6, 10, 15, 21)
 EXPORTS = ("emu_sgemm", "emu_dgemm", "emu_set_stream", "emu_set_split_mode",
            "emu_domain_status", "emu_last_error", "emu_release_workspace",
            "emu_workspace_bytes", "emu_split_f32", "emu_split_f64", "emu_profile_enable",
-           "emu_profile_read", "emu_set_split_scope", "emu_scale_exponents")
+           "emu_profile_read", "emu_set_split_scope", "emu_scale_exponents", "emu_sgemm_ex",
+           "emu_dgemm_ex")
 
 
 class EmuError(RuntimeError):
@@ -60,6 +62,9 @@ def lib() -> ctypes.CDLL:
         L.emu_set_stream.argtypes = [p]
         L.emu_set_split_mode.argtypes = [ci]
         L.emu_set_split_scope.argtypes = [ci]
+        ch, f32, f64 = ctypes.c_char, ctypes.c_float, ctypes.c_double
+        L.emu_sgemm_ex.argtypes = [ch, ch, i64, i64, i64, f32, p, i64, p, i64, f32, p, i64]
+        L.emu_dgemm_ex.argtypes = [ch, ch, i64, i64, i64, f64, p, i64, p, i64, f64, p, i64, ci]
         L.emu_scale_exponents.argtypes = [i64, i64, p, i64, ci, p]
         L.emu_domain_status.argtypes = [ctypes.POINTER(ctypes.c_uint)]
         L.emu_last_error.restype = ctypes.c_char_p
@@ -71,7 +76,8 @@ def lib() -> ctypes.CDLL:
         for name in ("emu_sgemm", "emu_dgemm", "emu_set_stream", "emu_set_split_mode",
                      "emu_domain_status", "emu_release_workspace", "emu_split_f32",
                      "emu_split_f64", "emu_profile_enable", "emu_profile_read",
-                     "emu_set_split_scope", "emu_scale_exponents"):
+                     "emu_set_split_scope", "emu_scale_exponents", "emu_sgemm_ex",
+                     "emu_dgemm_ex"):
             getattr(L, name).restype = ci
         _lib = L
     return _lib
@@ -131,6 +137,44 @@ def dgemm(A: torch.Tensor, B: torch.Tensor, nprod: int,
     _check(lib().emu_dgemm(M, N, K, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), C.data_ptr(),
                            _ld(C), int(nprod)))
     return C
+
+
+def _op_shape(X: torch.Tensor, trans: str):
+    if trans not in ("N", "T"):
+        raise ValueError("trans must be 'N' or 'T'")
+    return (X.shape[1], X.shape[0]) if trans == "T" else tuple(X.shape)
+
+
+def _gemm_ex(fn, dtype, A, B, C, transa, transb, alpha, beta, extra=()):
+    _mat(A, dtype, "A")
+    _mat(B, dtype, "B")
+    M, K = _op_shape(A, transa)
+    K2, N = _op_shape(B, transb)
+    if K != K2:
+        raise ValueError("inner dimensions differ")
+    if C is None:
+        if beta != 0:
+            raise ValueError("beta != 0 needs C")
+        C = torch.empty((M, N), dtype=dtype, device=A.device)
+    _mat(C, dtype, "C")
+    if tuple(C.shape) != (M, N):
+        raise ValueError("C must be M x N")
+    _bind_stream(A.device)
+    _check(fn(transa.encode(), transb.encode(), M, N, K, alpha, A.data_ptr(), _ld(A),
+              B.data_ptr(), _ld(B), beta, C.data_ptr(), _ld(C), *extra))
+    return C
+
+
+def sgemm_ex(A, B, C=None, transa="N", transb="N", alpha=1.0, beta=0.0):
+    """C = alpha op(A) op(B) + beta C in FP32 (A, B as stored; see emu.h)."""
+    return _gemm_ex(lib().emu_sgemm_ex, torch.float32, A, B, C, transa, transb, float(alpha),
+                    float(beta))
+
+
+def dgemm_ex(A, B, nprod, C=None, transa="N", transb="N", alpha=1.0, beta=0.0):
+    """C = alpha op(A) op(B) + beta C in FP64 with nprod retained products."""
+    return _gemm_ex(lib().emu_dgemm_ex, torch.float64, A, B, C, transa, transb, float(alpha),
+                    float(beta), (int(nprod),))
 
 
 def split_f32(X: torch.Tensor, as_b: bool = False) -> torch.Tensor:

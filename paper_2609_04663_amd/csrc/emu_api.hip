@@ -135,15 +135,25 @@ int nprod_to_d(int nprod) {
     }
 }
 
-// Validation shared by both GEMMs (Sec. 3.2 problem statement, row-major).
-int check_gemm_args(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B,
-                    int64_t ldb, const void *C, int64_t ldc) {
+// Validation shared by both GEMMs (Sec. 3.2 problem statement, row-major, with
+// the BLAS transposition flags: op(A) is M x K, op(B) is K x N).
+int trans_flag(char t, bool *tr) {
+    switch (t) {
+        case 'N': case 'n': *tr = false; return EMU_OK;
+        case 'T': case 't': case 'C': case 'c': *tr = true; return EMU_OK;
+        default: return fail(EMU_EINVAL, "transa / transb must be 'N' or 'T'");
+    }
+}
+
+int check_gemm_args(bool ta, bool tb, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
+                    const void *B, int64_t ldb, const void *C, int64_t ldc, bool need_ab) {
     if (M < 0 || N < 0 || K < 0) return fail(EMU_EINVAL, "M, N and K must be non-negative");
-    if (lda < (K > 1 ? K : 1)) return fail(EMU_EINVAL, "lda < max(1, K)");
-    if (ldb < (N > 1 ? N : 1)) return fail(EMU_EINVAL, "ldb < max(1, N)");
+    const int64_t acols = ta ? M : K, bcols = tb ? K : N;
+    if (lda < (acols > 1 ? acols : 1)) return fail(EMU_EINVAL, ta ? "lda < max(1, M)" : "lda < max(1, K)");
+    if (ldb < (bcols > 1 ? bcols : 1)) return fail(EMU_EINVAL, tb ? "ldb < max(1, K)" : "ldb < max(1, N)");
     if (ldc < (N > 1 ? N : 1)) return fail(EMU_EINVAL, "ldc < max(1, N)");
     if (M > 0 && N > 0 && !C) return fail(EMU_EINVAL, "C is NULL");
-    if (M > 0 && N > 0 && K > 0 && (!A || !B)) return fail(EMU_EINVAL, "A or B is NULL");
+    if (need_ab && M > 0 && N > 0 && K > 0 && (!A || !B)) return fail(EMU_EINVAL, "A or B is NULL");
     if (M > (int64_t)1 << 31 || N > (int64_t)1 << 31 || K > (int64_t)1 << 36)
         return fail(EMU_EINVAL, "matrix dimension too large");
     return EMU_OK;
@@ -259,43 +269,59 @@ int emu_domain_status(unsigned *flags) {
     return EMU_OK;
 }
 
-int emu_sgemm(int64_t M, int64_t N, int64_t K, const float *A, int64_t lda, const float *B,
-              int64_t ldb, float *C, int64_t ldc) {
-    int rc = check_gemm_args(M, N, K, A, lda, B, ldb, C, ldc);
+int emu_sgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, float alpha,
+                 const float *A, int64_t lda, const float *B, int64_t ldb, float beta, float *C,
+                 int64_t ldc) {
+    bool ta = false, tb = false;
+    int rc = trans_flag(transa, &ta);
+    if (!rc) rc = trans_flag(transb, &tb);
+    if (!rc) rc = check_gemm_args(ta, tb, M, N, K, A, lda, B, ldb, C, ldc, alpha != 0.0f);
     if (rc) return rc;
     g_err.clear();
     if (M == 0 || N == 0) return EMU_OK;
-    if (K == 0) {
-        hipError_t e = launch_fill_f32(C, M, N, ldc, g_stream);
-        return e == hipSuccess ? EMU_OK : hip_fail(e, "fill");
+    if (K == 0 || alpha == 0.0f) {
+        hipError_t e = launch_scale_c_f32(C, M, N, ldc, beta, g_stream);
+        return e == hipSuccess ? EMU_OK : hip_fail(e, "scale C");
     }
     const Shape s = plan(M, N, K, 3, SGEMM_MT, SGEMM_NT);
     rc = ensure_workspace(s.bytesA + s.bytesB);
     if (rc) return rc;
     uint16_t *Ap = ws_planes(0), *Bp = ws_planes(s.bytesA);
     prof_mark(0);
-    hipError_t e = launch_split_f32(A, M, K, lda, false, Ap, s.KB, s.RpadA, ws_status(), g_stream);
+    // op(A) rows are A's rows ('N') or A's columns ('T': A is K x M, packed as a B operand)
+    hipError_t e = ta ? launch_split_f32(A, K, M, lda, true, Ap, s.KB, s.RpadA, ws_status(), g_stream)
+                      : launch_split_f32(A, M, K, lda, false, Ap, s.KB, s.RpadA, ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f32(A)");
-    e = launch_split_f32(B, K, N, ldb, true, Bp, s.KB, s.RpadB, ws_status(), g_stream);
+    e = tb ? launch_split_f32(B, N, K, ldb, false, Bp, s.KB, s.RpadB, ws_status(), g_stream)
+           : launch_split_f32(B, K, N, ldb, true, Bp, s.KB, s.RpadB, ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f32(B)");
     prof_mark(1);
-    e = launch_gemm_f32(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, g_stream);
+    e = launch_gemm_f32(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, alpha, beta, g_stream);
     if (e != hipSuccess) return hip_fail(e, "gemm_f32");
     prof_mark(2);
     return EMU_OK;
 }
 
-int emu_dgemm(int64_t M, int64_t N, int64_t K, const double *A, int64_t lda, const double *B,
-              int64_t ldb, double *C, int64_t ldc, int nprod) {
+int emu_sgemm(int64_t M, int64_t N, int64_t K, const float *A, int64_t lda, const float *B,
+              int64_t ldb, float *C, int64_t ldc) {
+    return emu_sgemm_ex('N', 'N', M, N, K, 1.0f, A, lda, B, ldb, 0.0f, C, ldc);
+}
+
+int emu_dgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, double alpha,
+                 const double *A, int64_t lda, const double *B, int64_t ldb, double beta,
+                 double *C, int64_t ldc, int nprod) {
     const int d = nprod_to_d(nprod);
     if (d < 0) return fail(EMU_EINVAL, "nprod must be 6, 10, 15 or 21");
-    int rc = check_gemm_args(M, N, K, A, lda, B, ldb, C, ldc);
+    bool ta = false, tb = false;
+    int rc = trans_flag(transa, &ta);
+    if (!rc) rc = trans_flag(transb, &tb);
+    if (!rc) rc = check_gemm_args(ta, tb, M, N, K, A, lda, B, ldb, C, ldc, alpha != 0.0);
     if (rc) return rc;
     g_err.clear();
     if (M == 0 || N == 0) return EMU_OK;
-    if (K == 0) {
-        hipError_t e = launch_fill_f64(C, M, N, ldc, g_stream);
-        return e == hipSuccess ? EMU_OK : hip_fail(e, "fill");
+    if (K == 0 || alpha == 0.0) {
+        hipError_t e = launch_scale_c_f64(C, M, N, ldc, beta, g_stream);
+        return e == hipSuccess ? EMU_OK : hip_fail(e, "scale C");
     }
     // Only the d slices the retained products read are materialised; the
     // levels after them never influence slices 0 .. d-1.
@@ -306,27 +332,34 @@ int emu_dgemm(int64_t M, int64_t N, int64_t K, const double *A, int64_t lda, con
     uint16_t *Ap = ws_planes(0), *Bp = ws_planes(s.bytesA);
     F64SplitState *st = ws_states();
     const ScaleArea sc = ws_scales(s.bytesA + s.bytesB, M, N);
+    // stored shapes: A is M x K ('N') or K x M ('T'); B is K x N ('N') or N x K ('T')
+    const int64_t ar = ta ? K : M, ac = ta ? M : K, br = tb ? N : K, bc = tb ? K : N;
     prof_mark(0);
     hipError_t e = hipSuccess;
     if (scaled) {
-        // weights: rows of A, columns of B (the scale-aware split)
-        e = launch_scale_exponents(A, M, K, lda, false, sc.mb, sc.sa, g_stream);
+        // weights: rows of op(A), columns of op(B) (the scale-aware split)
+        e = launch_scale_exponents(A, ar, ac, lda, ta, sc.mb, sc.sa, g_stream);
         if (e != hipSuccess) return hip_fail(e, "scale_exponents(A)");
-        e = launch_scale_exponents(B, K, N, ldb, true, sc.mb + M, sc.sb, g_stream);
+        e = launch_scale_exponents(B, br, bc, ldb, !tb, sc.mb + M, sc.sb, g_stream);
         if (e != hipSuccess) return hip_fail(e, "scale_exponents(B)");
     }
-    e = launch_split_f64(A, M, K, lda, false, scaled ? sc.sa : nullptr, Ap, s.KB, s.RpadA, d,
+    e = launch_split_f64(A, ar, ac, lda, ta, scaled ? sc.sa : nullptr, Ap, s.KB, s.RpadA, d,
                          g_split_mode, st, ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f64(A)");
-    e = launch_split_f64(B, K, N, ldb, true, scaled ? sc.sb : nullptr, Bp, s.KB, s.RpadB, d,
+    e = launch_split_f64(B, br, bc, ldb, !tb, scaled ? sc.sb : nullptr, Bp, s.KB, s.RpadB, d,
                          g_split_mode, st + 1, ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f64(B)");
     prof_mark(1);
     e = launch_gemm_f64(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, scaled ? sc.sa : nullptr,
-                        scaled ? sc.sb : nullptr, d, g_stream);
+                        scaled ? sc.sb : nullptr, alpha, beta, d, g_stream);
     if (e != hipSuccess) return hip_fail(e, "gemm_f64");
     prof_mark(2);
     return EMU_OK;
+}
+
+int emu_dgemm(int64_t M, int64_t N, int64_t K, const double *A, int64_t lda, const double *B,
+              int64_t ldb, double *C, int64_t ldc, int nprod) {
+    return emu_dgemm_ex('N', 'N', M, N, K, 1.0, A, lda, B, ldb, 0.0, C, ldc, nprod);
 }
 
 static int check_split_args(int64_t R, int64_t Cc, const void *X, int64_t ldx, int as_b,

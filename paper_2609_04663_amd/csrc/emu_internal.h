@@ -69,6 +69,10 @@ constexpr int V_ZERO = (int)0x80000000;   // level whose residual is identically
 namespace emu {
 hipError_t launch_fill_f32(float *C, int64_t M, int64_t N, int64_t ldc, hipStream_t s);
 hipError_t launch_fill_f64(double *C, int64_t M, int64_t N, int64_t ldc, hipStream_t s);
+hipError_t launch_scale_c_f32(float *C, int64_t M, int64_t N, int64_t ldc, float beta,
+                              hipStream_t s);
+hipError_t launch_scale_c_f64(double *C, int64_t M, int64_t N, int64_t ldc, double beta,
+                              hipStream_t s);
 hipError_t launch_split_f32(const float *X, int64_t rows, int64_t cols, int64_t ldx, bool as_b,
                             uint16_t *P, int64_t KB, int64_t Rpad, unsigned *status,
                             hipStream_t s);
@@ -83,11 +87,14 @@ hipError_t launch_scale_exponents(const double *X, int64_t rows, int64_t cols, i
 hipError_t launch_unpack(const uint16_t *P, int nc, int64_t KB, int64_t Rpad, int64_t rows,
                          int64_t cols, bool as_b, uint16_t *out, hipStream_t s);
 hipError_t launch_copy_v(const F64SplitState *st, int32_t *v, hipStream_t s);
+// alpha, beta: C = alpha P + beta C (see out_update); 1, 0 stores P
 hipError_t launch_gemm_f32(const uint16_t *Ap, const uint16_t *Bp, float *C, int64_t M, int64_t N,
-                           int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc, hipStream_t s);
+                           int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc, float alpha,
+                           float beta, hipStream_t s);
 // sa, sb: row weights of A and column weights of B to restore (C_mn times
 // 2^(sa_m + sb_n)), or both null
 hipError_t launch_gemm_f64(const uint16_t *Ap, const uint16_t *Bp, double *C, int64_t M,
                            int64_t N, int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc,
-                           const int *sa, const int *sb, int d, hipStream_t s);
+                           const int *sa, const int *sb, double alpha, double beta, int d,
+                           hipStream_t s);
 }  // namespace emu

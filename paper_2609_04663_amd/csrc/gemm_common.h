@@ -103,6 +103,26 @@ __device__ inline void static_for(F &&f) {
 // their program order.
 __device__ inline void order_fence() { __builtin_amdgcn_sched_barrier(0x6); }
 
+// Output update of the BLAS form C = alpha P + beta C, rounded as
+// fl(fl(alpha P) + fl(beta C)) with no contraction; beta == 0 never reads C
+// (BLAS convention: C may hold anything), and alpha == 1, beta == 0 stores P.
+// (The operations are written here, under the pragma, rather than through
+// helper functions whose inlined bodies would still be contracted.)
+__device__ inline double out_update(double p, double alpha, double beta, const double *c) {
+#pragma clang fp contract(off)
+    const double ap = alpha * p;
+    if (beta == 0.0) return ap;
+    const double bc = beta * *c;
+    return ap + bc;
+}
+__device__ inline float out_update(float p, float alpha, float beta, const float *c) {
+#pragma clang fp contract(off)
+    const float ap = alpha * p;
+    if (beta == 0.0f) return ap;
+    const float bc = beta * *c;
+    return ap + bc;
+}
+
 // Output coordinates of accumulator register r of lane l in a 32x32 block:
 // row (r / 4) * 8 + (l / 32) * 4 + r % 4, column l % 32.
 __device__ inline int acc_row(int lane, int r) { return (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3); }

@@ -32,7 +32,8 @@ constexpr int B_CHUNKS = NC * B_BYTES / 1024;       // 24
 
 __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
     const uint16_t *__restrict__ Ap, const uint16_t *__restrict__ Bp, float *__restrict__ C,
-    int64_t M, int64_t N, int KB, int64_t RpadA, int64_t RpadB, int64_t ldc, int nt_m, int nt_n) {
+    int64_t M, int64_t N, int KB, int64_t RpadA, int64_t RpadB, int64_t ldc, float alpha,
+    float beta, int nt_m, int nt_n) {
     __shared__ __attribute__((aligned(1024))) char stage0[STAGE];
     __shared__ __attribute__((aligned(1024))) char stage1[STAGE];
 
@@ -192,7 +193,8 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int64_t row = m0 + wm * 32 * RB + rb * 32 + acc_row(lane, r);
-                if (row < M && col < N) C[row * ldc + col] = blk[rb][cb][r];
+                if (row < M && col < N)
+                    C[row * ldc + col] = out_update(blk[rb][cb][r], alpha, beta, C + row * ldc + col);
             }
         }
 }
@@ -200,10 +202,11 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
 }  // namespace
 
 hipError_t launch_gemm_f32(const uint16_t *Ap, const uint16_t *Bp, float *C, int64_t M, int64_t N,
-                           int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc, hipStream_t s) {
+                           int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc, float alpha,
+                           float beta, hipStream_t s) {
     const int nt_m = (int)((M + MT - 1) / MT), nt_n = (int)((N + NT - 1) / NT);
-    gemm_f32_kernel<<<nt_m * nt_n, 256, 0, s>>>(Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc, nt_m,
-                                               nt_n);
+    gemm_f32_kernel<<<nt_m * nt_n, 256, 0, s>>>(Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc, alpha,
+                                               beta, nt_m, nt_n);
     return hipGetLastError();
 }
 

@@ -83,7 +83,8 @@ template <int D, int BM, int NS, bool ACC64_LDS, int AFTER>
 __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
     const uint16_t *__restrict__ Ap, const uint16_t *__restrict__ Bp, double *__restrict__ C,
     int64_t M, int64_t N, int KB, int64_t RpadA, int64_t RpadB, int64_t ldc,
-    const int *__restrict__ sa, const int *__restrict__ sb, int nt_m, int nt_n) {
+    const int *__restrict__ sa, const int *__restrict__ sb, double alpha, double beta, int nt_m,
+    int nt_n) {
     using K = Cfg<D, BM, NS, ACC64_LDS, AFTER>;
     __shared__ __attribute__((aligned(1024))) char lds[K::NSTAGE * K::STAGE + K::ACC64_BYTES];
     // lane-private FP64 accumulators in LDS: element r of lane l of wave w at
@@ -286,7 +287,7 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
                 double val = ACC64_LDS ? acc64_lds[((wave * BM + b) * 16 + r) * 64 + lane]
                                        : acc64[ACC64_LDS ? 0 : b][r];
                 if (sa != nullptr) val = ldexp(val, sa[row] + col_w);
-                C[row * ldc + col] = val;
+                C[row * ldc + col] = out_update(val, alpha, beta, C + row * ldc + col);
             }
         }
     }
@@ -295,11 +296,11 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
 template <int D, int BM, int NS, bool ACC64_LDS, int AFTER>
 hipError_t launch_t(const uint16_t *Ap, const uint16_t *Bp, double *C, int64_t M, int64_t N,
                     int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc, const int *sa,
-                    const int *sb, hipStream_t s) {
+                    const int *sb, double alpha, double beta, hipStream_t s) {
     using K = Cfg<D, BM, NS, ACC64_LDS, AFTER>;
     const int nt_m = (int)((M + K::MT - 1) / K::MT), nt_n = (int)((N + K::NT - 1) / K::NT);
     gemm_f64_kernel<D, BM, NS, ACC64_LDS, AFTER><<<nt_m * nt_n, 256, 0, s>>>(Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc,
-                                                       sa, sb, nt_m, nt_n);
+                                                       sa, sb, alpha, beta, nt_m, nt_n);
     return hipGetLastError();
 }
 
@@ -307,12 +308,13 @@ hipError_t launch_t(const uint16_t *Ap, const uint16_t *Bp, double *C, int64_t M
 
 hipError_t launch_gemm_f64(const uint16_t *Ap, const uint16_t *Bp, double *C, int64_t M,
                            int64_t N, int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc,
-                           const int *sa, const int *sb, int d, hipStream_t s) {
+                           const int *sa, const int *sb, double alpha, double beta, int d,
+                           hipStream_t s) {
     switch (d) {
-        case 3: return launch_t<3, 2, 3, false, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, s);
-        case 4: return launch_t<4, 1, 3, false, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, s);
-        case 5: return launch_t<5, 1, 3, true, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, s);
-        case 6: return launch_t<6, 1, 2, true, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, s);
+        case 3: return launch_t<3, 2, 3, false, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
+        case 4: return launch_t<4, 1, 3, false, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
+        case 5: return launch_t<5, 1, 3, true, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
+        case 6: return launch_t<6, 1, 2, true, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
         default: return hipErrorInvalidValue;
     }
 }

@@ -413,6 +413,29 @@ int grid_for_pairs(int64_t npairs) {
 
 }  // namespace
 
+// C = beta C (0 when beta == 0: C is then not read), the BLAS result when
+// alpha == 0 or K == 0.
+template <typename T>
+__global__ void scale_c_kernel(T *C, int64_t M, int64_t N, int64_t ldc, T beta) {
+    for (int64_t r = blockIdx.x; r < M; r += gridDim.x)
+        for (int64_t c = threadIdx.x; c < N; c += blockDim.x)
+            C[r * ldc + c] = (beta == T(0)) ? T(0) : beta * C[r * ldc + c];
+}
+
+hipError_t launch_scale_c_f32(float *C, int64_t M, int64_t N, int64_t ldc, float beta,
+                              hipStream_t s) {
+    const int g = (int)(M < 4096 ? (M > 0 ? M : 1) : 4096);
+    scale_c_kernel<float><<<g, 256, 0, s>>>(C, M, N, ldc, beta);
+    return hipGetLastError();
+}
+
+hipError_t launch_scale_c_f64(double *C, int64_t M, int64_t N, int64_t ldc, double beta,
+                              hipStream_t s) {
+    const int g = (int)(M < 4096 ? (M > 0 ? M : 1) : 4096);
+    scale_c_kernel<double><<<g, 256, 0, s>>>(C, M, N, ldc, beta);
+    return hipGetLastError();
+}
+
 hipError_t launch_fill_f32(float *C, int64_t M, int64_t N, int64_t ldc, hipStream_t s) {
     const int g = (int)(M < 4096 ? M : 4096);
     fill_zero_kernel<float><<<g, 256, 0, s>>>(C, M, N, ldc);

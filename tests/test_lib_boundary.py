@@ -103,3 +103,25 @@ def test_split_scope_and_scale_hook_arguments(L):
     assert L.emu_scale_exponents(4, 4, None, 4, 0, P) == emu.EMU_EINVAL    # NULL X
     assert L.emu_scale_exponents(4, 4, P, 4, 1, None) == emu.EMU_EINVAL    # NULL s
     assert L.emu_scale_exponents(0, 4, None, 4, 0, None) == emu.EMU_OK     # nothing to do
+
+
+@pytest.mark.parametrize("ta,tb,args", [
+    (b"X", b"N", (4, 4, 4, 1.0, P, 4, P, 4, 0.0, P, 4)),      # bad transa
+    (b"N", b"Q", (4, 4, 4, 1.0, P, 4, P, 4, 0.0, P, 4)),      # bad transb
+    (b"T", b"N", (8, 4, 4, 1.0, P, 4, P, 4, 0.0, P, 4)),      # A^T: lda < M
+    (b"N", b"T", (4, 4, 8, 1.0, P, 8, P, 7, 0.0, P, 4)),      # B^T: ldb < K
+    (b"N", b"N", (4, 8, 4, 1.0, P, 4, P, 8, 0.0, P, 7)),      # ldc < N
+    (b"T", b"T", (-1, 4, 4, 1.0, P, 4, P, 4, 0.0, P, 4)),     # negative M
+    (b"N", b"N", (4, 4, 4, 1.0, None, 4, P, 4, 0.0, P, 4)),   # NULL A with alpha != 0
+])
+def test_blas_forms_invalid_arguments(L, ta, tb, args):
+    import paper_2609_04663_amd as emu
+    assert L.emu_sgemm_ex(ta, tb, *args) == emu.EMU_EINVAL
+    assert L.emu_dgemm_ex(ta, tb, *args, 6) == emu.EMU_EINVAL
+
+
+def test_blas_forms_empty_output_and_nprod(L):
+    import paper_2609_04663_amd as emu
+    assert L.emu_sgemm_ex(b"T", b"T", 0, 4, 4, 1.0, P, 1, P, 4, 0.0, P, 4) == emu.EMU_OK
+    assert L.emu_dgemm_ex(b"n", b"t", 4, 0, 4, 1.0, P, 4, P, 4, 0.0, P, 1, 21) == emu.EMU_OK
+    assert L.emu_dgemm_ex(b"N", b"N", 4, 4, 4, 1.0, P, 4, P, 4, 0.0, P, 4, 7) == emu.EMU_EINVAL
