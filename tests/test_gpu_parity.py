@@ -308,3 +308,42 @@ def test_workspace_limit_gives_enomem(emu):
         del os.environ["EMU_WORKSPACE_LIMIT"]
     C = emu.sgemm(dev(np.ones((30, 30), np.float32)), dev(np.ones((30, 30), np.float32)))
     assert torch.all(C == 30).item()
+
+
+# ---------------------------------------------------------------------------
+# degenerate operands of the method
+
+
+@pytest.mark.parametrize("nprod", [6, 21])
+def test_dgemm_zero_and_single_entry_operands(emu, nprod):
+    """A = 0 gives all-zero slices (the zero-residual rule) and C = 0; a single
+    nonzero entry gives its exact slices; both bit-exact with the oracle."""
+    B = S.make("wide", 341, (300, 70), np.float64)
+    A = np.zeros((90, 300))
+    C = emu.dgemm(dev(A), dev(B), nprod).cpu().numpy()
+    assert not C.any()
+    A[17, 123] = -3.0e-5
+    ref, _ = O.emu_dgemm(A, B, nprod)
+    C = emu.dgemm(dev(A), dev(B), nprod).cpu().numpy()
+    assert np.array_equal(C, ref)
+
+
+@pytest.mark.parametrize("shape", [(1, 300, 5000), (300, 1, 5000), (1, 1, 70000)])
+def test_vector_shapes(emu, shape):
+    """GEMV-like shapes and a long single dot product (many panels)."""
+    M, N, K = shape
+    A = S.make("wide", 351, (M, K), np.float64)
+    B = S.make("uniform", 352, (K, N), np.float64)
+    ref, _ = O.emu_dgemm(A, B, 10)
+    assert np.array_equal(emu.dgemm(dev(A), dev(B), 10).cpu().numpy(), ref)
+    A32, B32 = A.astype(np.float32), B.astype(np.float32)
+    if M * N >= 64:
+        check_sgemm(emu, A32, B32)
+    else:
+        # one output number: the ratio to the oracle's error is a single sample
+        # (here about 2x either way), so only the absolute bounds of R5 apply
+        Cg = emu.sgemm(dev(A32), dev(B32)).cpu().numpy()
+        ref64 = O.ref_gemm_f64(A32, B32)
+        esc, _ = O.e_scaled(Cg, ref64, np.abs(A32.astype(np.float64)) @ np.abs(B32.astype(np.float64)))
+        ef_cap, esc_cap = sgemm_bounds(K)
+        assert O.e_F(Cg, ref64) <= ef_cap and esc <= esc_cap
