@@ -46,7 +46,8 @@ SCOPE_ROWCOL = 1
 KC = 256  # reduction-panel length B_K of the paper's blocked loop (Sec. 6.1)
 
 ST_NAN, ST_RANGE, ST_SUBNORMAL, ST_OVERFLOW, ST_INEXACT32 = 1, 2, 4, 8, 16
-NPROD_TO_D = {6: 3, 10: 4, 15: 5, 21: 6}
+# N_p(d) = |S_d| of Eq. (product-selection), six slices per operand, d = 1 .. 11
+NPROD_TO_D = {sum(1 for i in range(6) for j in range(6) if i + j < d): d for d in range(1, 12)}
 
 
 def compile_source(src: str, out: str) -> str:

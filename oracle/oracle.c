@@ -402,14 +402,18 @@ unsigned orc_emu_sgemm_entries(i64 M, i64 N, i64 K, const float *A, i64 lda, con
 /* ------------------------------------------------------------------------- */
 /* Emulated DGEMM, Algorithm fp64 / Eq. (fp64reconstruction). */
 
+/* N_p(d) = |S_d| of Eq. (product-selection) with six slices per operand,
+   S_d = {(i, j) : 0 <= i, j < 6, i + j < d}, for d = 1 .. 11 (d = 11 keeps all
+   36 products); the paper evaluates d = 3 .. 6 (Eq. fp64productcounts). */
 static int nprod_to_d(int nprod) {
-    switch (nprod) {
-        case 6: return 3;
-        case 10: return 4;
-        case 15: return 5;
-        case 21: return 6;
-        default: return -1;
+    for (int d = 1; d <= 11; ++d) {
+        int n = 0;
+        for (int i = 0; i < 6; ++i)
+            for (int j = 0; j < 6; ++j)
+                if (i + j < d) ++n;
+        if (n == nprod) return d;
     }
+    return -1;
 }
 
 static double dgemm_entry(i64 K, i64 kc, int d, const uint16_t *Av, const uint16_t *Bv, i64 M,
@@ -420,6 +424,7 @@ static double dgemm_entry(i64 K, i64 kc, int d, const uint16_t *Av, const uint16
         for (int l = 0; l < d; ++l) {               /* diagonal l = i + j */
             for (int i = 0; i <= l; ++i) {
                 int j = l - i;
+                if (i > 5 || j > 5) continue;       /* six slices per operand */
                 const uint16_t *Ai = Av + (size_t)i * M * K + (size_t)m * K;
                 const uint16_t *Bj = Bv + (size_t)j * K * N + n;
                 xacc x;

@@ -82,7 +82,7 @@ def test_dgemm_integers_give_exact_product(nprod):
     assert st == 0 and np.array_equal(C.astype(np.int64), exact)
 
 
-@pytest.mark.parametrize("nprod", [6, 10, 15, 21])
+@pytest.mark.parametrize("nprod", [1, 3, 6, 10, 15, 21, 26, 36])
 def test_dgemm_identity_sums_retained_slices(nprod):
     d = O.NPROD_TO_D[nprod]
     A = S.make("uniform", 8, (5, 260), np.float64)
@@ -91,10 +91,10 @@ def test_dgemm_identity_sums_retained_slices(nprod):
     for i in range(5):
         for j in range(260):
             c = Fraction(0)
-            for r in range(d):                      # products (r, 0), diagonal r
+            for r in range(min(d, 6)):              # products (r, 0), diagonal r
                 c = _round64(c + bf16_value(slices[r, i, j]))
             assert Fraction(float(C[i, j])) == c
-    if d == 6:
+    if d >= 6:
         assert np.array_equal(C, A - resid) or np.max(np.abs(C - (A - resid))) <= 2.0 ** -53
 
 
@@ -130,7 +130,7 @@ def test_sgemm_definition_bruteforce(shape):
             assert Fraction(float(C[m, n])) == blk, (m, n)
 
 
-@pytest.mark.parametrize("nprod", [6, 21])
+@pytest.mark.parametrize("nprod", [1, 3, 6, 21, 30, 36])
 @pytest.mark.parametrize("shape", [(3, 4, 5), (2, 3, 520)])
 def test_dgemm_definition_bruteforce(nprod, shape):
     M, N, K = shape
@@ -146,7 +146,7 @@ def test_dgemm_definition_bruteforce(nprod, shape):
             c = Fraction(0)
             for p0 in range(0, K, 256):
                 for ell in range(d):
-                    for i in range(ell + 1):
+                    for i in range(max(0, ell - 5), min(ell, 5) + 1):
                         j = ell - i
                         P = sum(bf16_value(sa[i, m, k]) * bf16_value(sb[j, k, n])
                                 for k in range(p0, min(K, p0 + 256)))
@@ -155,14 +155,16 @@ def test_dgemm_definition_bruteforce(nprod, shape):
             assert Fraction(float(C[m, n])) == c, (m, n)
 
 
-def test_dgemm_definition_bruteforce_order_sensitive():
-    """K = 1 and all 21 products: the FP64 chain spans more than 53 bits, so the
-    roundings of the last diagonals depend on the order of the additions
+@pytest.mark.parametrize("nprod", [21, 36])
+def test_dgemm_definition_bruteforce_order_sensitive(nprod):
+    """K = 1 and 21 or all 36 products: the FP64 chain spans more than 53 bits,
+    so the roundings of the last diagonals depend on the order of the additions
     (diagonal ascending, i ascending): 4096 entries against exact products
     added in that order in Python floats (IEEE binary64)."""
+    d = O.NPROD_TO_D[nprod]
     A = S.make("wide", 43, (64, 1), np.float64)
     B = S.make("wide", 44, (1, 64), np.float64)
-    C, st = O.emu_dgemm(A, B, 21)
+    C, st = O.emu_dgemm(A, B, nprod)
     assert st == 0
     sa, _, _, _ = O.split_f64(A)
     sb, _, _, _ = O.split_f64(B)
@@ -171,8 +173,8 @@ def test_dgemm_definition_bruteforce_order_sensitive():
     for m in range(64):
         for n in range(64):
             c = 0.0
-            for ell in range(6):
-                for i in range(ell + 1):
+            for ell in range(d):
+                for i in range(max(0, ell - 5), min(ell, 5) + 1):
                     c = c + av[i, m] * bv[ell - i, n]     # exact product (<= 16 bits)
             assert C[m, n] == c, (m, n)
 

@@ -12,6 +12,7 @@ import os
 import pytest
 
 import oracle as O
+import test_oracle_depths as DP
 import test_oracle_gemm as G
 import test_oracle_split as SP
 
@@ -59,14 +60,26 @@ MUTATIONS = {
         "for (int l = 0; l <= d && l < 6; ++l) {     /* diagonal l = i + j */",
         [lambda: G.test_dgemm_identity_sums_retained_slices(6),
          lambda: G.test_table_accuracy_fp64_columns(256)]),
+    "dgemm_selection_drops_sixth_slice": (
+        "if (i > 5 || j > 5) continue;       /* six slices per operand */",
+        "if (i > 4 || j > 4) continue;       /* six slices per operand */",
+        [lambda: DP.test_structured_operands_closed_form(7)]),
+    "dgemm_selection_inclusive_bound": (
+        "for (int l = 0; l < d; ++l) {               /* diagonal l = i + j */",
+        "for (int l = 0; l <= d; ++l) {              /* diagonal l = i + j */",
+        [lambda: DP.test_structured_operands_closed_form(6)]),
+    "dgemm_product_count_map_shifted": (
+        "if (i + j < d) ++n;",
+        "if (i + j <= d) ++n;",
+        [lambda: DP.test_structured_operands_closed_form(1), lambda: DP.test_other_product_counts_rejected(2)]),
     "dgemm_order_inside_diagonal_reversed": (
         "for (int i = 0; i <= l; ++i) {\n                int j = l - i;",
         "for (int i = l; i >= 0; --i) {\n                int j = l - i;",
-        [G.test_dgemm_definition_bruteforce_order_sensitive]),
+        [lambda: G.test_dgemm_definition_bruteforce_order_sensitive(21)]),
     "dgemm_slice_index_transposed": (
         "const uint16_t *Ai = Av + (size_t)i * M * K + (size_t)m * K;\n                const uint16_t *Bj = Bv + (size_t)j * K * N + n;",
         "const uint16_t *Ai = Av + (size_t)j * M * K + (size_t)m * K;\n                const uint16_t *Bj = Bv + (size_t)i * K * N + n;",
-        [G.test_dgemm_definition_bruteforce_order_sensitive]),
+        [lambda: G.test_dgemm_definition_bruteforce_order_sensitive(21)]),
     "dgemm_accumulates_in_fp32": (
         "c = c + (double)p32;                /* widen exactly, add in FP64 */",
         "c = (double)((float)c + p32);",
