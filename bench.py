@@ -14,8 +14,9 @@ before the timed region.
 Prints one JSON line.  Also reported: per-variant phase times from HIP events
 recorded by the library on its stream (split/pack vs GEMM, the analog of the
 paper's runtime breakdown), the roofline object of the dominant kernel, a
-sampled parity check against the CPU oracle, and the oracle itself timed on the
-host cores as a baseline.
+sampled parity check against the CPU oracle, the oracle itself timed on the
+host cores as a baseline, and, as context outside the step, the other product
+counts of the selection sequence (nprod 1, 3 and 26 .. 36) on the same inputs.
 """
 import argparse
 import hashlib
@@ -97,6 +98,8 @@ def main():
                          "scale-aware row/column weights")
     ap.add_argument("--no-native", action="store_true",
                     help="skip timing the vendor library's native FP32/FP64 GEMM (context)")
+    ap.add_argument("--no-depths", action="store_true",
+                    help="skip the context timing of the other product counts (nprod 1, 3, 26..36)")
     ap.add_argument("--print-source-hash", action="store_true",
                     help="print the source hash of each GEMM kernel and exit")
     args = ap.parse_args()
@@ -182,6 +185,31 @@ def main():
                   "bf16_tflops": round(lib_rate(dA32.to(torch.bfloat16), dB32.to(torch.bfloat16), 5), 2),
                   "library": "torch.matmul (hipBLASLt/rocBLAS), same inputs (bf16: RNE-cast)"}
 
+    # context: the rest of the selection sequence S_d (d = 1, 2, 7 .. 11) on the
+    # same FP64 inputs, one warm-up and three profiled calls each
+    depths = None
+    if not args.no_depths:
+        log("bench: other product counts for context")
+        depths = {}
+        Cx = torch.empty((n, n), dtype=torch.float64, device="cuda")   # not the step's outputs
+        for p in (1, 3, 26, 30, 33, 35, 36):
+            emu.dgemm(dA64, dB64, p, C=Cx)
+            torch.cuda.synchronize()
+            emu.profile_enable(True)
+            emu.profile_read()
+            for _ in range(3):
+                emu.dgemm(dA64, dB64, p, C=Cx)
+            torch.cuda.synchronize()
+            s_ms, g_ms = emu.profile_read()
+            emu.profile_enable(False)
+            s_m, g_m = float(np.mean(s_ms)), float(np.mean(g_ms))
+            depths[str(p)] = {
+                "effective_tflops": round(2.0 * n ** 3 / ((s_m + g_m) * 1e-3) / 1e12, 2),
+                "split_ms": round(s_m, 4), "gemm_ms": round(g_m, 4),
+                "mfma_frac": round(p * 2.0 * n ** 3 / (g_m * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+        status |= emu.domain_status()
+        del Cx
+
     flop = 2.0 * n ** 3
     elapsed = t1 - t0
     value = len(VARIANTS) * flop * args.steps / elapsed / 1e12
@@ -209,6 +237,10 @@ def main():
         native["emu_dgemm_speedup_vs_native_fp64"] = {
             str(p): round(per_variant[f"emu-DGEMM-{p}"]["effective_tflops"] / native["fp64_tflops"], 3)
             for p in (6, 10, 15, 21)}
+        if depths:
+            # headroom: the same GEMM kernel with one product (A_0 B_0, FP64
+            # output) against the vendor bf16 GEMM, both as bf16 MFMA fractions
+            native["same_kernel_nprod1_gemm_frac_of_peak"] = depths["1"]["mfma_frac"]
     # dominant kernel: the GEMM launch with the largest share of the step
     dom = max(range(len(VARIANTS)), key=lambda i: np.mean(gemm_ms[i::len(VARIANTS)]))
     kind, p = VARIANTS[dom]
@@ -216,7 +248,9 @@ def main():
     achieved = p * flop / (g_avg * 1e-3) / 1e12
     kkey = f"{kind}:{p}:{n}"
     roofline = {
-        "kernel": ("gemm_f32_kernel" if kind == "sgemm" else f"gemm_f64_kernel<d={ {6: 3, 10: 4, 15: 5, 21: 6}[p]}>"),
+        "kernel": ("gemm_f32_kernel" if kind == "sgemm" else
+                   "gemm_f64w_kernel<d=6>" if p == 21 else
+                   f"gemm_f64_kernel<d={ {6: 3, 10: 4, 15: 5}[p]}>"),
         "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
         "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
         "traffic": traffic_for(kkey),
@@ -285,6 +319,7 @@ def main():
         "context_peaks_tflops": {"bf16_mfma": PEAK_BF16_TFLOPS, "fp32_matrix": PEAK_FP32_MATRIX,
                                  "fp64_matrix": PEAK_FP64_MATRIX},
         "context_native_gemm": native,
+        "context_other_depths": depths,
         "context_paper_8192": PAPER_CONTEXT_8192 if n == 8192 else None,
     }
     print(json.dumps(line), flush=True)

@@ -21,9 +21,9 @@
  * Return codes.  EMU_OK on success.  EMU_EINVAL for a bad argument (checked
  * before any HIP call, nothing is launched): M, N or K negative; lda < K,
  * ldb < N, ldc < N (each at least 1); a NULL pointer for an operand with a
- * nonzero extent; nprod not in {6, 10, 15, 21}.  EMU_EHIP when a HIP runtime
- * call or kernel launch fails (message in emu_last_error).  EMU_ENOMEM when the
- * workspace cannot be allocated.
+ * nonzero extent; nprod not one of the N_p(d) listed at emu_dgemm.  EMU_EHIP
+ * when a HIP runtime call or kernel launch fails (message in emu_last_error).
+ * EMU_ENOMEM when the workspace cannot be allocated.
  *
  * Degenerate sizes.  M == 0 or N == 0: nothing is done.  K == 0: C = 0.
  *
@@ -90,10 +90,13 @@ int emu_sgemm(int64_t M, int64_t N, int64_t K, const float *A, int64_t lda, cons
 
 /* Emulated DGEMM, Algorithm fp64 (Sec. 4.3, Eq. fp64split, fp64productcounts,
    fp64reconstruction): each FP64 operand gets the fixed six-slice Ozaki split
-   with operand-wide exponents; the nprod products with i + j < d
-   (nprod = 6, 10, 15, 21 for d = 3, 4, 5, 6) are each formed in FP32 per
-   reduction panel of 256 (exactly, see below), widened and added in FP64 in
-   the order: panel ascending, diagonal i + j ascending, i ascending.
+   with operand-wide exponents; the nprod products A_i B_j with i, j < 6 and
+   i + j < d (Eq. product-selection) are each formed in FP32 per reduction
+   panel of 256 (exactly, see below), widened and added in FP64 in the order:
+   panel ascending, diagonal i + j ascending, i ascending.  nprod = N_p(d):
+   6, 10, 15, 21 for the paper's d = 3, 4, 5, 6 (Eq. fp64productcounts), and
+   the rest of the selection sequence, 1, 3 (d = 1, 2) and 26, 30, 33, 35, 36
+   (d = 7 .. 11; 36 keeps all six-by-six products, Sec. 4.3).
    A: M x K (lda), B: K x N (ldb), C: M x N (ldc), device pointers, FP64.
    For in-domain inputs every panel product is an exact FP32 value, so the
    result is independent of the order of the bf16 MFMA accumulation inside a

@@ -30,7 +30,10 @@ EMU_OK, EMU_EINVAL, EMU_EHIP, EMU_ENOMEM = 0, 1, 2, 3
 STATUS_NAN, STATUS_RANGE, STATUS_SUBNORMAL, STATUS_OVERFLOW = 1, 2, 4, 8
 SPLIT_SYM, SPLIT_LITERAL = 0, 1
 SCOPE_OPERAND, SCOPE_ROWCOL = 0, 1
+# the paper's product counts N_p(d), d = 3 .. 6 (Eq. fp64productcounts) ...
 NPROD = (6, 10, 15, 21)
+# ... and every depth d = 1 .. 11 of the selection S_d (Eq. product-selection)
+NPROD_ALL = (1, 3, 6, 10, 15, 21, 26, 30, 33, 35, 36)
 
 EXPORTS = ("emu_sgemm", "emu_dgemm", "emu_set_stream", "emu_set_split_mode",
            "emu_domain_status", "emu_last_error", "emu_release_workspace",

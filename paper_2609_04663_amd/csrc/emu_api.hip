@@ -125,14 +125,13 @@ ScaleArea ws_scales(size_t planes_bytes, int64_t nA, int64_t nB) {
     return a;
 }
 
+// Depth d of the triangular selection S_d = {(i, j) : i, j < 6, i + j < d}
+// (Eq. product-selection) with N_p(d) = |S_d| = nprod, or -1.
 int nprod_to_d(int nprod) {
-    switch (nprod) {
-        case 6: return 3;
-        case 10: return 4;
-        case 15: return 5;
-        case 21: return 6;
-        default: return -1;
-    }
+    static const int count[12] = {0, 1, 3, 6, 10, 15, 21, 26, 30, 33, 35, 36};
+    for (int d = 1; d <= 11; ++d)
+        if (count[d] == nprod) return d;
+    return -1;
 }
 
 // Validation shared by both GEMMs (Sec. 3.2 problem statement, row-major, with
@@ -311,7 +310,7 @@ int emu_dgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, doub
                  const double *A, int64_t lda, const double *B, int64_t ldb, double beta,
                  double *C, int64_t ldc, int nprod) {
     const int d = nprod_to_d(nprod);
-    if (d < 0) return fail(EMU_EINVAL, "nprod must be 6, 10, 15 or 21");
+    if (d < 0) return fail(EMU_EINVAL, "nprod must be 1, 3, 6, 10, 15, 21, 26, 30, 33, 35 or 36");
     bool ta = false, tb = false;
     int rc = trans_flag(transa, &ta);
     if (!rc) rc = trans_flag(transb, &tb);
@@ -323,9 +322,10 @@ int emu_dgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, doub
         hipError_t e = launch_scale_c_f64(C, M, N, ldc, beta, g_stream);
         return e == hipSuccess ? EMU_OK : hip_fail(e, "scale C");
     }
-    // Only the d slices the retained products read are materialised; the
-    // levels after them never influence slices 0 .. d-1.
-    const Shape s = plan(M, N, K, d, dgemm_mt(d), DGEMM_NT);
+    // Only the slices the retained products read are materialised; the levels
+    // after them never influence the earlier slices.
+    const int np = dgemm_planes(d);
+    const Shape s = plan(M, N, K, np, dgemm_mt(d), DGEMM_NT);
     const bool scaled = g_split_scope == EMU_SCOPE_ROWCOL;
     rc = ensure_workspace(s.bytesA + s.bytesB + (scaled ? scale_bytes(M, N) : 0));
     if (rc) return rc;
@@ -343,10 +343,10 @@ int emu_dgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, doub
         e = launch_scale_exponents(B, br, bc, ldb, !tb, sc.mb + M, sc.sb, g_stream);
         if (e != hipSuccess) return hip_fail(e, "scale_exponents(B)");
     }
-    e = launch_split_f64(A, ar, ac, lda, ta, scaled ? sc.sa : nullptr, Ap, s.KB, s.RpadA, d,
+    e = launch_split_f64(A, ar, ac, lda, ta, scaled ? sc.sa : nullptr, Ap, s.KB, s.RpadA, np,
                          g_split_mode, st, ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f64(A)");
-    e = launch_split_f64(B, br, bc, ldb, !tb, scaled ? sc.sb : nullptr, Bp, s.KB, s.RpadB, d,
+    e = launch_split_f64(B, br, bc, ldb, !tb, scaled ? sc.sb : nullptr, Bp, s.KB, s.RpadB, np,
                          g_split_mode, st + 1, ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f64(B)");
     prof_mark(1);

@@ -33,7 +33,9 @@ constexpr int KPANEL = 256;     // reduction panel B_K of the FP32/FP64 reconstr
 // ... and of the GEMM tile that reads them (output tile rows for A, columns for B).
 constexpr int SGEMM_MT = 192, SGEMM_NT = 128;
 constexpr int DGEMM_NT = 64;
-inline int dgemm_mt(int d) { return d == 3 ? 128 : 64; }
+inline int dgemm_mt(int d) { return d == 1 ? 256 : d <= 3 ? 128 : 64; }
+// Slices of each operand that the products of depth d read (indices < 6).
+inline int dgemm_planes(int d) { return d < 6 ? d : 6; }
 constexpr int KB_PER_PANEL = KPANEL / KBLK;
 
 __host__ __device__ inline int swz(int64_t row) { return (int)((row >> 2) & 3); }

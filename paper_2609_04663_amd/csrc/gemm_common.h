@@ -9,6 +9,7 @@ namespace emu {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void *lds_void_ptr;
 
 // Workgroup -> output tile.  The hardware hands workgroup i to XCD i % 8; the
@@ -73,6 +74,22 @@ __device__ inline void mfma_vacc_zero(f32x16 &c, bf16x8 a, bf16x8 b) {
 // (the hardware does not interlock this; 24 is above what a 32x32x16 MFMA
 // needs).  Taking c as an operand orders every later reader after it.
 __device__ inline void mfma_vacc_settle(f32x16 &c) {
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(c));
+}
+
+// The same for the 16 x 16 x 32 MFMA (lane l holds A row l % 16 and B column
+// l % 16 over reduction indices 8 (l / 16) .. 8 (l / 16) + 7; accumulator
+// register r of lane l is output row 4 (l / 16) + r, column l % 16).
+__device__ inline f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ inline void mfma16_vacc(f32x4 &c, bf16x8 a, bf16x8 b) {
+    asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(c) : "v"(a), "v"(b));
+}
+__device__ inline void mfma16_vacc_zero(f32x4 &c, bf16x8 a, bf16x8 b) {
+    asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, 0" : "=v"(c) : "v"(a), "v"(b));
+}
+__device__ inline void mfma16_vacc_settle(f32x4 &c) {
     asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" : "+v"(c));
 }
 

@@ -62,10 +62,19 @@ def test_gemm_invalid_arguments(L, args):
     assert L.emu_dgemm(*args, 10) == emu.EMU_EINVAL
 
 
-@pytest.mark.parametrize("nprod", [0, 1, 3, 7, 20, 36, -6])
+@pytest.mark.parametrize("nprod", [0, 2, 4, 7, 20, 22, 34, 37, -6])
 def test_dgemm_invalid_nprod(L, nprod):
     import paper_2609_04663_amd as emu
     assert L.emu_dgemm(4, 4, 4, P, 4, P, 4, P, 4, nprod) == emu.EMU_EINVAL
+
+
+def test_dgemm_accepts_every_depth(L):
+    """N_p(d) for d = 1 .. 11 pass validation (M = 0: no launch follows)."""
+    import paper_2609_04663_amd as emu
+    assert emu.NPROD_ALL == tuple(sum(1 for i in range(6) for j in range(6) if i + j < d)
+                                  for d in range(1, 12))
+    for nprod in emu.NPROD_ALL:
+        assert L.emu_dgemm(0, 4, 4, P, 4, P, 4, P, 4, nprod) == emu.EMU_OK
 
 
 def test_empty_output_is_a_no_op(L):
