@@ -13,11 +13,14 @@
 // is sized so that the three accumulator sets below (288 registers) leave the
 // register allocator room: 128 x 64 spills.
 //
-// Accumulation: A0B0 goes to one FP32 accumulator set, the five smaller
-// products to another; at the end of every reduction panel of 256 (the
-// paper's B_K, Sec. 6.1/6.3) the two are combined and added into an FP32 block
-// total.  Keeping the leading product apart stops the small products from
-// being rounded against the large partial sums inside the MFMA accumulator.
+// Accumulation: A0B0 goes to one FP32 accumulator set (hi), flushed into an
+// FP32 block total at the end of every reduction panel of 256 (the paper's
+// B_K, Sec. 6.1/6.3); the five smaller products go to another set (lo) that
+// runs over the whole reduction and is added to the block total at the end.
+// Keeping the leading product apart stops the small products from being
+// rounded against the large partial sums; lo itself is about 2^-8 of C, so
+// its own rounding over the full length stays far below FP32 level, and the
+// panel flush reads only hi (half the accumulator reads of flushing both).
 #include "gemm_common.h"
 
 namespace emu {
@@ -96,12 +99,14 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
     // of the next sub-step (stage nbase, lane offset noff) of the fragments whose
     // last use was MFMA t, then copy t / 2 of k-block ckb (even t, t / 2 < NCOPY).
     // Latency cover of every read: at least 12 MFMAs.
-    // zero: the panel's first sub-step (accumulators start at 0).
+    // zero: the panel's first sub-step (hi starts at 0); zero_lo: the first
+    // sub-step of the whole reduction (lo starts at 0).
     constexpr int PI[6] = {0, 0, 0, 1, 1, 2}, PJ[6] = {0, 1, 2, 0, 1, 0};
     auto step = [&](Frags &f, const bf16x8 (&b0)[2], bf16x8 (&b0n)[2], f32x16 (&hi)[RB][2],
-                    f32x16 (&lo)[RB][2], auto zero_c, const char *nbase, int noff, int ckb,
-                    char *cdst, auto ncopy_c) {
+                    f32x16 (&lo)[RB][2], auto zero_c, auto zero_lo_c, const char *nbase, int noff,
+                    int ckb, char *cdst, auto ncopy_c) {
         constexpr bool zero = decltype(zero_c)::value;
+        constexpr bool zero_lo = decltype(zero_lo_c)::value;
         constexpr int NCOPY = decltype(ncopy_c)::value;
         static_assert(RB == 3, "last-use slots below assume three row blocks");
         static_for<36>([&](auto t_c) {
@@ -112,7 +117,7 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
             if constexpr (g == 0)
                 hi[rb][cb] = mfma(f.a[0][rb], bop, zero ? f32x16{} : hi[rb][cb]);
             else
-                lo[rb][cb] = mfma(f.a[i][rb], bop, (zero && g == 1) ? f32x16{} : lo[rb][cb]);
+                lo[rb][cb] = mfma(f.a[i][rb], bop, (zero_lo && g == 1) ? f32x16{} : lo[rb][cb]);
             order_fence();
             // last uses: B0 -> second buffer at t = 0, 1; A0[r] at 13 + 2r; B2[c] at
             // 16 + c; A1[r] at 25 + 2r; B1[c] at 28 + c; A2[r] at 31 + 2r
@@ -159,27 +164,34 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
     b0a[0] = f.b[0][0];
     b0a[1] = f.b[0][1];
     int kb = 0;
+    f32x16 lo[RB][2];
     for (int p0 = 0; p0 < KB; p0 += KB_PER_PANEL) {
         const int p1 = min(KB, p0 + KB_PER_PANEL);
-        f32x16 hi[RB][2], lo[RB][2];
-        auto kblock = [&](auto first_c) {
+        f32x16 hi[RB][2];
+        auto kblock = [&](auto first_c, auto first_lo_c) {
             char *cur = (kb & 1) ? stage1 : stage0;
             char *nxt = (kb & 1) ? stage0 : stage1;
-            step(f, b0a, b0b, hi, lo, first_c, cur, off1, 0, cur, std::integral_constant<int, 0>{});
+            step(f, b0a, b0b, hi, lo, first_c, first_lo_c, cur, off1, 0, cur,
+                 std::integral_constant<int, 0>{});
             __builtin_amdgcn_sched_barrier(0);
             asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
             pipeline_barrier();
-            step(f, b0b, b0a, hi, lo, std::false_type{}, nxt, off0, min(kb + 2, KB - 1), cur,
-                 std::integral_constant<int, COPIES>{});
+            step(f, b0b, b0a, hi, lo, std::false_type{}, std::false_type{}, nxt, off0,
+                 min(kb + 2, KB - 1), cur, std::integral_constant<int, COPIES>{});
             __builtin_amdgcn_sched_barrier(0);
         };
-        kblock(std::true_type{});     // panel's first k-block: accumulators start at 0
-        for (++kb; kb < p1; ++kb) kblock(std::false_type{});
+        if (p0 == 0) kblock(std::true_type{}, std::true_type{});
+        else kblock(std::true_type{}, std::false_type{});
+        for (++kb; kb < p1; ++kb) kblock(std::false_type{}, std::false_type{});
 #pragma unroll
         for (int i = 0; i < RB; ++i)
 #pragma unroll
-            for (int j = 0; j < 2; ++j) blk[i][j] += lo[i][j] + hi[i][j];
+            for (int j = 0; j < 2; ++j) blk[i][j] += hi[i][j];
     }
+#pragma unroll
+    for (int i = 0; i < RB; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) blk[i][j] += lo[i][j];
     // the last trips issued (unused) copies: let them land before the workgroup
     // ends and its LDS is handed to another workgroup
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
