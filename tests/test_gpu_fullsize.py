@@ -131,6 +131,21 @@ def test_dgemm_wide(emu, n):
     torch.cuda.empty_cache()
 
 
+def test_dgemm_wide_8192_other_depths(emu):
+    """The rest of the selection sequence (Eq. product-selection) at the full
+    size: nprod 1 and 3 on the 32 x 32 kernel, 26 .. 36 on the 16 x 16 x 32
+    kernel (FP64 tile in registers for 26, in LDS from 30 on)."""
+    n = 8192
+    sa, sb = S.seeds(4)
+    A = S.make("wide", sa, (n, n), np.float64)
+    B = S.make("wide", sb, (n, n), np.float64)
+    emu.domain_status()
+    run_dgemm(emu, A, B, (1, 3, 26, 30, 33, 35, 36), seed=n + 7)
+    assert emu.domain_status() == 0
+    emu.release_workspace()
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("shape", [(16384, 16384, 512), (1024, 1024, 65536)])
 def test_rectangular_scaled_rows(emu, shape):
     M, N, K = shape
