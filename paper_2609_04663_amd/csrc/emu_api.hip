@@ -21,16 +21,16 @@ int g_split_mode = EMU_SPLIT_SYM;
 int g_split_scope = EMU_SCOPE_OPERAND;
 std::string g_err;
 
-// Workspace: [status word (offset 0), two FP64 split states (offset 128): 512 B]
-//            [operand A planes][operand B planes].
+// Workspace: [status word (offset 0), the FP64 split state slots of two
+//            operands (offset 128): 2 KB header][operand A planes][operand B planes].
 // Grown only when a call needs more; the status word is preserved across growth.
 struct Workspace {
     char *base = nullptr;
     size_t bytes = 0;
 } g_ws;
 
-constexpr size_t HDR = 512;
-static_assert(128 + 2 * sizeof(F64SplitState) <= HDR, "workspace header");
+constexpr size_t HDR = 2048;
+static_assert(128 + 2 * F64_SLOTS * sizeof(F64SplitState) <= HDR, "workspace header");
 
 int fail(int code, const char *msg) {
     g_err = msg;
@@ -287,13 +287,13 @@ int emu_sgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, floa
     if (rc) return rc;
     uint16_t *Ap = ws_planes(0), *Bp = ws_planes(s.bytesA);
     prof_mark(0);
-    // op(A) rows are A's rows ('N') or A's columns ('T': A is K x M, packed as a B operand)
-    hipError_t e = ta ? launch_split_f32(A, K, M, lda, true, Ap, s.KB, s.RpadA, ws_status(), g_stream)
-                      : launch_split_f32(A, M, K, lda, false, Ap, s.KB, s.RpadA, ws_status(), g_stream);
-    if (e != hipSuccess) return hip_fail(e, "split_f32(A)");
-    e = tb ? launch_split_f32(B, N, K, ldb, false, Bp, s.KB, s.RpadB, ws_status(), g_stream)
-           : launch_split_f32(B, K, N, ldb, true, Bp, s.KB, s.RpadB, ws_status(), g_stream);
-    if (e != hipSuccess) return hip_fail(e, "split_f32(B)");
+    // op(A) rows are A's rows ('N') or A's columns ('T': A is K x M, packed as a
+    // B operand); op(B) columns likewise; both operands in one launch
+    const F32SplitOperand ops[2] = {
+        {A, ta ? K : M, ta ? M : K, lda, ta ? 1 : 0, Ap, s.RpadA},
+        {B, tb ? N : K, tb ? K : N, ldb, tb ? 0 : 1, Bp, s.RpadB}};
+    hipError_t e = launch_split_f32(ops, 2, s.KB, ws_status(), g_stream);
+    if (e != hipSuccess) return hip_fail(e, "split_f32");
     prof_mark(1);
     e = launch_gemm_f32(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, alpha, beta, g_stream);
     if (e != hipSuccess) return hip_fail(e, "gemm_f32");
@@ -343,12 +343,13 @@ int emu_dgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, doub
         e = launch_scale_exponents(B, br, bc, ldb, !tb, sc.mb + M, sc.sb, g_stream);
         if (e != hipSuccess) return hip_fail(e, "scale_exponents(B)");
     }
-    e = launch_split_f64(A, ar, ac, lda, ta, scaled ? sc.sa : nullptr, Ap, s.KB, s.RpadA, np,
-                         g_split_mode, st, ws_status(), g_stream);
-    if (e != hipSuccess) return hip_fail(e, "split_f64(A)");
-    e = launch_split_f64(B, br, bc, ldb, !tb, scaled ? sc.sb : nullptr, Bp, s.KB, s.RpadB, np,
-                         g_split_mode, st + 1, ws_status(), g_stream);
-    if (e != hipSuccess) return hip_fail(e, "split_f64(B)");
+    // both operands in one launch per phase: op(A)'s rows are A's rows ('N') or
+    // A's columns ('T', packed as a B operand), op(B)'s columns likewise
+    const F64SplitOperand ops[2] = {
+        {A, ar, ac, lda, ta ? 1 : 0, scaled ? sc.sa : nullptr, Ap, s.RpadA, st},
+        {B, br, bc, ldb, tb ? 0 : 1, scaled ? sc.sb : nullptr, Bp, s.RpadB, st + F64_SLOTS}};
+    e = launch_split_f64(ops, 2, s.KB, np, g_split_mode, ws_status(), g_stream);
+    if (e != hipSuccess) return hip_fail(e, "split_f64");
     prof_mark(1);
     e = launch_gemm_f64(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, scaled ? sc.sa : nullptr,
                         scaled ? sc.sb : nullptr, alpha, beta, d, g_stream);
@@ -381,8 +382,8 @@ int emu_split_f32(int64_t R, int64_t Cc, const float *X, int64_t ldx, int as_b, 
     rc = ensure_workspace(s.bytesA);
     if (rc) return rc;
     uint16_t *P = ws_planes(0);
-    hipError_t e = launch_split_f32(X, R, Cc, ldx, as_b != 0, P, s.KB, s.RpadA, ws_status(),
-                                    g_stream);
+    const F32SplitOperand op = {X, R, Cc, ldx, as_b != 0 ? 1 : 0, P, s.RpadA};
+    hipError_t e = launch_split_f32(&op, 1, s.KB, ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f32");
     e = launch_unpack(P, 3, s.KB, s.RpadA, R, Cc, as_b != 0, comps, g_stream);
     if (e != hipSuccess) return hip_fail(e, "unpack");
@@ -408,8 +409,9 @@ int emu_split_f64(int64_t R, int64_t Cc, const double *X, int64_t ldx, int as_b,
         e = launch_scale_exponents(X, R, Cc, ldx, as_b != 0, sc.mb, sc.sa, g_stream);
         if (e != hipSuccess) return hip_fail(e, "scale_exponents");
     }
-    e = launch_split_f64(X, R, Cc, ldx, as_b != 0, scaled ? sc.sa : nullptr, P, s.KB, s.RpadA, 6,
-                         g_split_mode, st, ws_status(), g_stream);
+    const F64SplitOperand op = {X, R, Cc, ldx, as_b != 0 ? 1 : 0, scaled ? sc.sa : nullptr, P,
+                                s.RpadA, st};
+    e = launch_split_f64(&op, 1, s.KB, 6, g_split_mode, ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f64");
     if (R > 0 && Cc > 0) {
         e = launch_unpack(P, 6, s.KB, s.RpadA, R, Cc, as_b != 0, slices, g_stream);

@@ -50,10 +50,12 @@ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 // Status bits (same values as EMU_STATUS_* in emu.h).
 constexpr unsigned ST_NAN = 1u, ST_RANGE = 2u, ST_SUBNORMAL = 4u, ST_OVERFLOW = 8u;
 
-// Device state of one FP64 operand split: the operand-wide per-level maxima
-// (bit patterns of non-negative doubles, whose unsigned order is the numeric
-// order), the exponent chain v, and the first level a replay pass must
-// recompute (-1 when the chain is verified).
+// Device state of the FP64 split of one operand: the operand-wide per-level
+// maxima (bit patterns of non-negative doubles, whose unsigned order is the
+// numeric order), the exponent chain v, and the first level the pass that
+// wrote it recomputed (-1 once the chain is verified).  One slot per pass:
+// slot 0 holds the level-0 maximum, slot p + 1 the state after pass p, so a
+// pass only reads a slot that an earlier launch completed.
 struct alignas(64) F64SplitState {
     unsigned long long maxbits[6];
     int v[6];
@@ -61,6 +63,28 @@ struct alignas(64) F64SplitState {
     int nlev;
     int mode;
     int pad[3];
+};
+constexpr int F64_SLOTS = 7;    // nlev <= 6 passes
+
+// One operand of an FP32 split launch.
+struct F32SplitOperand {
+    const float *X;
+    int64_t rows, cols, ldx;    // X as stored
+    int as_b;                   // packed rows are X's columns (a B operand)
+    uint16_t *P;                // packed planes
+    int64_t Rpad;
+};
+
+// One operand of an FP64 split launch (the GEMM splits A and B in one launch
+// per phase).
+struct F64SplitOperand {
+    const double *X;
+    int64_t rows, cols, ldx;    // X as stored
+    int as_b;                   // packed rows are X's columns (a B operand)
+    const int *sc;              // per-packed-row weights 2^-sc (scale-aware split) or null
+    uint16_t *P;                // packed planes
+    int64_t Rpad;
+    F64SplitState *st;          // F64_SLOTS slots
 };
 
 constexpr int V_ZERO = (int)0x80000000;   // level whose residual is identically zero
@@ -75,13 +99,13 @@ hipError_t launch_scale_c_f32(float *C, int64_t M, int64_t N, int64_t ldc, float
                               hipStream_t s);
 hipError_t launch_scale_c_f64(double *C, int64_t M, int64_t N, int64_t ldc, double beta,
                               hipStream_t s);
-hipError_t launch_split_f32(const float *X, int64_t rows, int64_t cols, int64_t ldx, bool as_b,
-                            uint16_t *P, int64_t KB, int64_t Rpad, unsigned *status,
+// The FP32 split of nops <= 2 operands with the same KB, one launch.
+hipError_t launch_split_f32(const F32SplitOperand *ops, int nops, int64_t KB, unsigned *status,
                             hipStream_t s);
-// sc: per-packed-row weights 2^-sc of the scale-aware split, or null
-hipError_t launch_split_f64(const double *X, int64_t rows, int64_t cols, int64_t ldx, bool as_b,
-                            const int *sc, uint16_t *P, int64_t KB, int64_t Rpad, int nlev,
-                            int mode, F64SplitState *st, unsigned *status, hipStream_t s);
+// The FP64 split of nops <= 2 operands with the same KB: nlev <= 6 levels
+// (planes) each, 2 + nlev launches in all.
+hipError_t launch_split_f64(const F64SplitOperand *ops, int nops, int64_t KB, int nlev, int mode,
+                            unsigned *status, hipStream_t s);
 // per-row (by_col = 0) or per-column exponents ceil(log2 max|x|) of X; mb is
 // scratch of rows (or cols) 64-bit words
 hipError_t launch_scale_exponents(const double *X, int64_t rows, int64_t cols, int64_t ldx,

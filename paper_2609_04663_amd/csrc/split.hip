@@ -59,16 +59,19 @@ __device__ inline ItemCoords item_coords(int64_t pair, int RG) {
 // AS_B = false: X is rows x cols (an A operand, packed row = X row, k = col).
 // AS_B = true : X is rows x cols = K x N (a B operand, packed row = column n,
 //               k = X row), i.e. B is packed transposed.
+// Blocks [b0, b0 + nb) of the launch serve one operand, block b of them the
+// items b, b + nb, ...
 template <bool AS_B>
-__global__ __launch_bounds__(SPLIT_THREADS) void split_f32_kernel(
-    const float *__restrict__ X, int64_t rows, int64_t cols, int64_t ldx, u16 *__restrict__ P,
-    int64_t KB, int64_t Rpad, unsigned *__restrict__ status) {
+__device__ __forceinline__ void split_f32_operand(const float *__restrict__ X, int64_t rows,
+                                                  int64_t cols, int64_t ldx, u16 *__restrict__ P,
+                                                  int64_t KB, int64_t Rpad,
+                                                  unsigned *__restrict__ status, int b, int nb) {
     const int RG = (int)(Rpad / ROWS_PER_BLOCK);
     const int64_t npairs = KB * RG;
     const int64_t prow_lim = AS_B ? cols : rows;
     const int64_t k_lim = AS_B ? rows : cols;
     unsigned st = 0;
-    for (int64_t pair = blockIdx.x; pair < npairs; pair += gridDim.x) {
+    for (int64_t pair = b; pair < npairs; pair += nb) {
         const ItemCoords ic = item_coords(pair, RG);
         const int64_t k0 = ic.kb * KBLK + ic.q * 8;
         float x[8];
@@ -117,15 +120,39 @@ __global__ __launch_bounds__(SPLIT_THREADS) void split_f32_kernel(
     if ((threadIdx.x & 63) == 0 && st) atomicOr(status, st);
 }
 
+// Operands of one FP32 split launch (the GEMM splits A and B together).
+struct F32SplitArgs {
+    F32SplitOperand op[2];
+    int nops;
+    int blocks0;          // blocks of operand 0; the rest serve operand 1
+    int64_t KB;
+    unsigned *status;
+};
+
+__global__ __launch_bounds__(SPLIT_THREADS) void split_f32_kernel(F32SplitArgs a) {
+    const bool second = a.nops > 1 && (int)blockIdx.x >= a.blocks0;
+    const F32SplitOperand &op = second ? a.op[1] : a.op[0];
+    const int b = (int)blockIdx.x - (second ? a.blocks0 : 0);
+    const int nb = second ? (int)gridDim.x - a.blocks0 : a.blocks0;
+    if (op.as_b)
+        split_f32_operand<true>(op.X, op.rows, op.cols, op.ldx, op.P, a.KB, op.Rpad, a.status, b, nb);
+    else
+        split_f32_operand<false>(op.X, op.rows, op.cols, op.ldx, op.P, a.KB, op.Rpad, a.status, b, nb);
+}
+
 // ---------------------------------------------------------------------------
-// FP64 split state machine.  The operand-wide maximum of every level is a
-// global reduction; instead of six dependent passes the split speculates the
-// exponent chain v_(r+1) = v_r - step (step = 9 for the symmetric projection,
-// 8 for the literal one), records the true maxima of the residuals it
-// produces, and a verify step replays from the first level whose recorded
-// maximum contradicts the speculation.  Levels before the first mismatch were
-// computed with verified exponents, so the recorded maximum at the mismatch is
-// the true one; every replay fixes at least one more level.
+// FP64 split.  The operand-wide maximum of every level is a global reduction;
+// instead of six dependent passes the split speculates the exponent chain
+// v_(r+1) = v_r - step (step = 9 for the symmetric projection, 8 for the
+// literal one) and records the true maxima of the residuals it produces.  Each
+// later pass first verifies the chain against the maxima the previous pass
+// recorded, from the first unverified level on; at the first mismatch it
+// takes the recorded maximum (exact: every earlier level was computed with
+// verified exponents), re-speculates the levels after it and recomputes them.
+// Every pass fixes at least one more level, so nlev passes suffice; once the
+// chain is verified a pass only copies its state slot forward.  Every block
+// runs the (tiny) verification itself from the previous pass's slot, so no
+// separate launch is needed between passes.
 
 __device__ inline int ceil_log2_pos(double m) {
     int e;
@@ -137,72 +164,55 @@ __device__ inline unsigned long long dbits(double x) {
     return (unsigned long long)__double_as_longlong(x);
 }
 
-__global__ void f64_state_init(F64SplitState *st, int nst, int nlev, int mode) {
-    const int i = threadIdx.x;
-    if (i >= nst) return;
-    for (int r = 0; r < 6; ++r) { st[i].maxbits[r] = 0ull; st[i].v[r] = 0; }
-    st[i].replay_from = 0;
-    st[i].nlev = nlev;
-    st[i].mode = mode;
+// Operands of one launch and the split of its grid between them.
+struct F64SplitArgs {
+    F64SplitOperand op[2];
+    int nops;
+    int blocks0;          // blocks of operand 0; the rest serve operand 1
+    int64_t KB;
+    unsigned *status;
+};
+
+// The block's operand (selected, not indexed, so that the arguments stay in the
+// kernel-argument segment), its block index and block count within it.
+__device__ inline const F64SplitOperand &operand_of_block(const F64SplitArgs &a, int &b, int &nb) {
+    const bool second = a.nops > 1 && (int)blockIdx.x >= a.blocks0;
+    b = (int)blockIdx.x - (second ? a.blocks0 : 0);
+    nb = second ? (int)gridDim.x - a.blocks0 : a.blocks0;
+    return second ? a.op[1] : a.op[0];
 }
 
-__global__ void f64_state_speculate(F64SplitState *st, int nst) {
-    const int i = threadIdx.x;
-    if (i >= nst) return;
-    const int step = st[i].mode ? 8 : 9;
-    const double m0 = __longlong_as_double((long long)st[i].maxbits[0]);
-    const int v0 = (m0 == 0.0) ? V_ZERO : ceil_log2_pos(m0);
-    for (int r = 0; r < 6; ++r) {
-        st[i].v[r] = (v0 == V_ZERO) ? V_ZERO : v0 - step * r;
-        if (r > 0) st[i].maxbits[r] = 0ull;
-    }
-    st[i].replay_from = 0;
+__global__ void f64_state_init(F64SplitArgs a, int nlev, int mode) {
+    const int t = threadIdx.x;
+    if (t >= a.nops * F64_SLOTS) return;
+    F64SplitState &s = a.op[t / F64_SLOTS].st[t % F64_SLOTS];
+    for (int r = 0; r < 6; ++r) { s.maxbits[r] = 0ull; s.v[r] = 0; }
+    s.replay_from = 0;
+    s.nlev = nlev;
+    s.mode = mode;
 }
 
-__global__ void f64_state_verify(F64SplitState *st, int nst) {
-    const int i = threadIdx.x;
-    if (i >= nst) return;
-    F64SplitState &s = st[i];
-    const int step = s.mode ? 8 : 9;
-    const int start = s.replay_from < 0 ? s.nlev : s.replay_from + 1;
-    s.replay_from = -1;
-    for (int r = start; r < s.nlev; ++r) {
-        if (s.v[r - 1] == V_ZERO) { s.v[r] = V_ZERO; continue; }
-        const double m = __longlong_as_double((long long)s.maxbits[r]);
-        if (m == 0.0) {
-            for (int t = r; t < 6; ++t) s.v[t] = V_ZERO;
-            break;
-        }
-        const int vt = ceil_log2_pos(m);
-        if (vt == s.v[r]) continue;
-        s.v[r] = vt;
-        for (int t = r + 1; t < 6; ++t) { s.v[t] = vt - step * (t - r); s.maxbits[t] = 0ull; }
-        s.replay_from = r;
-        break;
-    }
-}
-
-// max |x| over an operand (level-0 maximum) and the input-domain checks of
-// Eq. (bf16rangefp64).  Rows are strided over blocks, columns over threads.
-// With weights (sc non-null) the operand is read as x 2^-sc[p], p the packed
-// row of x (X's row, or X's column when by_col), and the checks apply to it.
-__global__ __launch_bounds__(SPLIT_THREADS) void f64_maxabs_kernel(
-    const double *__restrict__ X, int64_t rows, int64_t cols, int64_t ldx,
-    const int *__restrict__ sc, int by_col, F64SplitState *__restrict__ st,
-    unsigned *__restrict__ status) {
+// max |x| over an operand (level-0 maximum, into slot 0) and the input-domain
+// checks of Eq. (bf16rangefp64).  Rows are strided over the operand's blocks,
+// columns over threads.  With weights (sc non-null) the operand is read as
+// x 2^-sc[p], p the packed row of x (X's row, or X's column for a B operand),
+// and the checks apply to it.
+__global__ __launch_bounds__(SPLIT_THREADS) void f64_maxabs_kernel(F64SplitArgs a) {
     __shared__ unsigned long long red[SPLIT_THREADS / 64];
+    int b, nb;
+    const F64SplitOperand &op = operand_of_block(a, b, nb);
     double m = 0.0;
     unsigned flags = 0;
     const double lo = 0x1p-126, hi = 0x1.fep127;   // (2 - 2^-7) 2^127
-    for (int64_t r = blockIdx.x; r < rows; r += gridDim.x) {
-        const double *row = X + r * ldx;
-        for (int64_t c = threadIdx.x; c < cols; c += SPLIT_THREADS) {
+    for (int64_t r = b; r < op.rows; r += nb) {
+        const double *row = op.X + r * op.ldx;
+        for (int64_t c = threadIdx.x; c < op.cols; c += SPLIT_THREADS) {
             double x = row[c];
-            if (sc) x = ldexp(x, -sc[by_col ? c : r]);
-            const double a = fabs(x);
+            if (op.sc) x = ldexp(x, -op.sc[op.as_b ? c : r]);
+            const double ax = fabs(x);
             if (!__builtin_isfinite(x)) { flags |= ST_NAN; continue; }
-            if (x != 0.0 && (a < lo || a > hi)) flags |= ST_RANGE;
-            if (a > m) m = a;
+            if (x != 0.0 && (ax < lo || ax > hi)) flags |= ST_RANGE;
+            if (ax > m) m = ax;
         }
     }
     for (int off = 32; off > 0; off >>= 1) m = fmax(m, __shfl_xor(m, off));
@@ -210,58 +220,52 @@ __global__ __launch_bounds__(SPLIT_THREADS) void f64_maxabs_kernel(
     const int w = threadIdx.x >> 6;
     if ((threadIdx.x & 63) == 0) {
         red[w] = dbits(m);
-        if (flags) atomicOr(status, flags);
+        if (flags) atomicOr(a.status, flags);
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        unsigned long long b = red[0];
-        for (int i = 1; i < SPLIT_THREADS / 64; ++i) b = red[i] > b ? red[i] : b;
-        if (b) atomicMax(&st->maxbits[0], b);
+        unsigned long long bm = red[0];
+        for (int i = 1; i < SPLIT_THREADS / 64; ++i) bm = red[i] > bm ? red[i] : bm;
+        if (bm) atomicMax(&op.st[0].maxbits[0], bm);
     }
 }
 
-// One speculative (first_pass) or replay pass of the six-slice split:
+// Pass `pass` of the six-slice split of every operand of the launch:
 //   Z = fl64(fl64(A^(r) + Sigma) - Sigma), Sigma = c 2^(v_r + 45)
 //   (c = 0.75 symmetric, 1 literal), A_r = fl_BF16(Z) (= Z in the domain),
 //   A^(r+1) = fl64(A^(r) - A_r); zero slices for a level whose residual is 0.
-// Writes slices r >= first recomputed level, records max|A^(r+1)| of the
-// levels after it.  nlev <= 6 levels are computed (the GEMM never reads
-// slices >= d, and they do not influence slices < d).
+// Reads slot `pass`, writes slot pass + 1: the chain it used, the first level
+// r0 it recomputed (its slices r >= r0 are rewritten) and the maxima
+// max|A^(r+1)| of the levels after r0.  nlev <= 6 levels are computed (the
+// GEMM never reads slices >= nlev, and they do not influence slices < nlev).
 template <bool AS_B>
-__global__ __launch_bounds__(SPLIT_THREADS) void split_f64_kernel(
-    const double *__restrict__ X, int64_t rows, int64_t cols, int64_t ldx,
-    const int *__restrict__ sc, u16 *__restrict__ P, int64_t KB, int64_t Rpad,
-    F64SplitState *__restrict__ stp, unsigned *__restrict__ status, int first_pass) {
+__device__ __forceinline__ void split_f64_pass(const F64SplitOperand op, int64_t KB, int b, int nb,
+                               const int (&v)[6], int r0, int nlev, double cst,
+                               F64SplitState *out, unsigned *status) {
     __shared__ unsigned long long red[6][SPLIT_THREADS / 64];
-    const int r0 = first_pass ? 0 : stp->replay_from;
-    if (r0 < 0) return;                                   // verified: nothing to redo
-    const int nlev = stp->nlev;
-    int v[6];
     double sig[6];
-    const double cst = stp->mode ? 1.0 : 0.75;
 #pragma unroll
-    for (int r = 0; r < 6; ++r) {
-        v[r] = stp->v[r];
-        sig[r] = (v[r] == V_ZERO) ? 0.0 : ldexp(cst, v[r] + 45);
-    }
+    for (int r = 0; r < 6; ++r) sig[r] = (v[r] == V_ZERO) ? 0.0 : ldexp(cst, v[r] + 45);
     double mx[6] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
     unsigned st = 0;
-    const int RG = (int)(Rpad / ROWS_PER_BLOCK);
+    const int RG = (int)(op.Rpad / ROWS_PER_BLOCK);
     const int64_t npairs = KB * RG;
-    const int64_t prow_lim = AS_B ? cols : rows;
-    const int64_t k_lim = AS_B ? rows : cols;
-    for (int64_t pair = blockIdx.x; pair < npairs; pair += gridDim.x) {
+    const int64_t prow_lim = AS_B ? op.cols : op.rows;
+    const int64_t k_lim = AS_B ? op.rows : op.cols;
+    const double *X = op.X;
+    const int64_t ldx = op.ldx;
+    for (int64_t pair = b; pair < npairs; pair += nb) {
         const ItemCoords ic = item_coords(pair, RG);
         const int64_t k0 = ic.kb * KBLK + ic.q * 8;
         double x[8];
-        const int wexp = (sc && ic.prow < prow_lim) ? -sc[ic.prow] : 0;   // row weight 2^-s
+        const int wexp = (op.sc && ic.prow < prow_lim) ? -op.sc[ic.prow] : 0;   // weight 2^-s
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const bool ok = ic.prow < prow_lim && k0 + i < k_lim;
             x[i] = ok ? (AS_B ? X[(k0 + i) * ldx + ic.prow] : X[ic.prow * ldx + k0 + i]) : 0.0;
-            if (sc) x[i] = ldexp(x[i], wexp);
+            if (op.sc) x[i] = ldexp(x[i], wexp);
         }
-        u16x8 out[6];
+        u16x8 outp[6];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             double w = x[i];
@@ -276,18 +280,18 @@ __global__ __launch_bounds__(SPLIT_THREADS) void split_f64_kernel(
                     st |= classify(h, z != 0.0);
                     w = w - (double)bf16_to_float(h);
                 }
-                out[r][i] = h;
+                outp[r][i] = h;
                 if (r + 1 < nlev && r >= r0) {
-                    const double a = fabs(w);
-                    if (a > mx[r + 1]) mx[r + 1] = a;
+                    const double ax = fabs(w);
+                    if (ax > mx[r + 1]) mx[r + 1] = ax;
                 }
             }
         }
 #pragma unroll
         for (int r = 0; r < 6; ++r)
             if (r >= r0 && r < nlev)
-                *reinterpret_cast<u16x8 *>(P + packed_index(r, ic.kb, ic.prow, ic.q, KB, Rpad)) =
-                    out[r];
+                *reinterpret_cast<u16x8 *>(op.P + packed_index(r, ic.kb, ic.prow, ic.q, KB, op.Rpad)) =
+                    outp[r];
     }
     // operand-wide maxima of the recomputed levels
     const int w = threadIdx.x >> 6;
@@ -303,11 +307,71 @@ __global__ __launch_bounds__(SPLIT_THREADS) void split_f64_kernel(
     if (threadIdx.x < 6 && threadIdx.x >= 1) {
         const int r = threadIdx.x;
         if (r > r0 && r < nlev) {
-            unsigned long long b = red[r][0];
-            for (int i = 1; i < SPLIT_THREADS / 64; ++i) b = red[r][i] > b ? red[r][i] : b;
-            if (b) atomicMax(&stp->maxbits[r], b);
+            unsigned long long bm = red[r][0];
+            for (int i = 1; i < SPLIT_THREADS / 64; ++i) bm = red[r][i] > bm ? red[r][i] : bm;
+            if (bm) atomicMax(&out->maxbits[r], bm);
         }
     }
+}
+
+__global__ __launch_bounds__(SPLIT_THREADS) void split_f64_kernel(F64SplitArgs a, int pass) {
+    int b, nb;
+    const F64SplitOperand &op = operand_of_block(a, b, nb);
+    const F64SplitState &in = op.st[pass];
+    F64SplitState *out = op.st + pass + 1;
+    const int nlev = in.nlev, step = in.mode ? 8 : 9;
+    int v[6];
+    unsigned long long mb[6];
+    int r0 = -1;
+#pragma unroll
+    for (int r = 0; r < 6; ++r) { v[r] = in.v[r]; mb[r] = in.maxbits[r]; }
+    if (pass == 0) {
+        // speculate the whole chain from the level-0 maximum
+        const double m0 = __longlong_as_double((long long)mb[0]);
+        const int v0 = (m0 == 0.0) ? V_ZERO : ceil_log2_pos(m0);
+#pragma unroll
+        for (int r = 0; r < 6; ++r) v[r] = (v0 == V_ZERO) ? V_ZERO : v0 - step * r;
+        r0 = 0;
+    } else {
+        // verify the levels after the previous pass's first recomputed level
+        // (compile-time level indices keep v and mb in registers)
+        const int rf = in.replay_from;
+        bool done = rf < 0;
+#pragma unroll
+        for (int r = 1; r < 6; ++r) {
+            if (done || r <= rf || r >= nlev) continue;
+            if (v[r - 1] == V_ZERO) { v[r] = V_ZERO; continue; }
+            const double m = __longlong_as_double((long long)mb[r]);
+            if (m == 0.0) {
+#pragma unroll
+                for (int t = r; t < 6; ++t) v[t] = V_ZERO;
+                done = true;
+                continue;
+            }
+            const int vt = ceil_log2_pos(m);
+            if (vt == v[r]) continue;
+            v[r] = vt;
+#pragma unroll
+            for (int t = r + 1; t < 6; ++t) v[t] = vt - step * (t - r);
+            r0 = r;
+            done = true;
+        }
+    }
+    if (b == 0 && threadIdx.x == 0) {
+        // levels <= r0 keep their maxima (all of them once verified); the
+        // levels after r0 are filled by this pass's atomics
+        for (int r = 0; r < 6; ++r) {
+            out->v[r] = v[r];
+            if (r0 < 0 || r <= r0) out->maxbits[r] = mb[r];
+        }
+        out->replay_from = r0;
+        out->nlev = nlev;
+        out->mode = in.mode;
+    }
+    if (r0 < 0) return;                                   // verified: nothing to redo
+    const double cst = in.mode ? 1.0 : 0.75;
+    if (op.as_b) split_f64_pass<true>(op, a.KB, b, nb, v, r0, nlev, cst, out, a.status);
+    else split_f64_pass<false>(op, a.KB, b, nb, v, r0, nlev, cst, out, a.status);
 }
 
 // ---------------------------------------------------------------------------
@@ -396,8 +460,9 @@ __global__ void unpack_kernel(const u16 *__restrict__ P, int nc, int64_t KB, int
     }
 }
 
+// The verified chain: the slot written by the last pass.
 __global__ void copy_v_kernel(const F64SplitState *st, int32_t *v) {
-    if (threadIdx.x < 6) v[threadIdx.x] = st->v[threadIdx.x];
+    if (threadIdx.x < 6) v[threadIdx.x] = st[st[0].nlev].v[threadIdx.x];
 }
 
 template <typename T>
@@ -448,38 +513,39 @@ hipError_t launch_fill_f64(double *C, int64_t M, int64_t N, int64_t ldc, hipStre
     return hipGetLastError();
 }
 
-hipError_t launch_split_f32(const float *X, int64_t rows, int64_t cols, int64_t ldx, bool as_b,
-                            uint16_t *P, int64_t KB, int64_t Rpad, unsigned *status,
+hipError_t launch_split_f32(const F32SplitOperand *ops, int nops, int64_t KB, unsigned *status,
                             hipStream_t s) {
-    const int g = grid_for_pairs(KB * (Rpad / ROWS_PER_BLOCK));
-    if (as_b)
-        split_f32_kernel<true><<<g, SPLIT_THREADS, 0, s>>>(X, rows, cols, ldx, P, KB, Rpad, status);
-    else
-        split_f32_kernel<false><<<g, SPLIT_THREADS, 0, s>>>(X, rows, cols, ldx, P, KB, Rpad, status);
+    if (nops < 1 || nops > 2) return hipErrorInvalidValue;
+    F32SplitArgs a{};
+    for (int o = 0; o < nops; ++o) a.op[o] = ops[o];
+    a.nops = nops;
+    a.KB = KB;
+    a.status = status;
+    a.blocks0 = grid_for_pairs(KB * (ops[0].Rpad / ROWS_PER_BLOCK));
+    const int g = a.blocks0 + (nops > 1 ? grid_for_pairs(KB * (ops[1].Rpad / ROWS_PER_BLOCK)) : 0);
+    split_f32_kernel<<<g, SPLIT_THREADS, 0, s>>>(a);
     return hipGetLastError();
 }
 
-// Full FP64 split of one operand: init, level-0 maximum, speculative pass,
-// then verify/replay until every level is verified (at most nlev - 1 replays,
-// each a no-op once the chain is verified), then a final verify.
-hipError_t launch_split_f64(const double *X, int64_t rows, int64_t cols, int64_t ldx, bool as_b,
-                            const int *sc, uint16_t *P, int64_t KB, int64_t Rpad, int nlev,
-                            int mode, F64SplitState *st, unsigned *status, hipStream_t s) {
-    f64_state_init<<<1, 64, 0, s>>>(st, 1, nlev, mode);
-    const int gm = (int)(rows < 2048 ? (rows > 0 ? rows : 1) : 2048);
-    f64_maxabs_kernel<<<gm, SPLIT_THREADS, 0, s>>>(X, rows, cols, ldx, sc, as_b ? 1 : 0, st, status);
-    f64_state_speculate<<<1, 64, 0, s>>>(st, 1);
-    const int g = grid_for_pairs(KB * (Rpad / ROWS_PER_BLOCK));
-    for (int pass = 0; pass < nlev; ++pass) {
-        if (pass > 0) f64_state_verify<<<1, 64, 0, s>>>(st, 1);
-        if (as_b)
-            split_f64_kernel<true><<<g, SPLIT_THREADS, 0, s>>>(X, rows, cols, ldx, sc, P, KB, Rpad,
-                                                                st, status, pass == 0);
-        else
-            split_f64_kernel<false><<<g, SPLIT_THREADS, 0, s>>>(X, rows, cols, ldx, sc, P, KB, Rpad,
-                                                                 st, status, pass == 0);
-    }
-    f64_state_verify<<<1, 64, 0, s>>>(st, 1);
+// Full FP64 split of the operands: init, level-0 maxima, then nlev passes (the
+// first speculative; each later one verifies, and replays only on a mismatch).
+hipError_t launch_split_f64(const F64SplitOperand *ops, int nops, int64_t KB, int nlev, int mode,
+                            unsigned *status, hipStream_t s) {
+    if (nops < 1 || nops > 2 || nlev < 1 || nlev > 6) return hipErrorInvalidValue;
+    F64SplitArgs a{};
+    for (int o = 0; o < nops; ++o) a.op[o] = ops[o];
+    a.nops = nops;
+    a.KB = KB;
+    a.status = status;
+    f64_state_init<<<1, 64, 0, s>>>(a, nlev, mode);
+    auto max_blocks = [](int64_t rows) { return (int)(rows < 2048 ? (rows > 0 ? rows : 1) : 2048); };
+    a.blocks0 = max_blocks(ops[0].rows);
+    const int gm = a.blocks0 + (nops > 1 ? max_blocks(ops[1].rows) : 0);
+    f64_maxabs_kernel<<<gm, SPLIT_THREADS, 0, s>>>(a);
+    a.blocks0 = grid_for_pairs(KB * (ops[0].Rpad / ROWS_PER_BLOCK));
+    const int g = a.blocks0 + (nops > 1 ? grid_for_pairs(KB * (ops[1].Rpad / ROWS_PER_BLOCK)) : 0);
+    for (int pass = 0; pass < nlev; ++pass)
+        split_f64_kernel<<<g, SPLIT_THREADS, 0, s>>>(a, pass);
     return hipGetLastError();
 }
 

@@ -94,7 +94,15 @@ def _f64_cases():
     ints = rng.integers(-2 ** 15, 2 ** 15 + 1, (40, 70)).astype(np.float64)
     single = np.zeros((33, 65))
     single[5, 7] = 1.0 / 3.0
+    # magnitude classes 22 bits apart with 7-bit mantissas: each level's
+    # maximum comes from the next class, so the speculated chain (9 bits per
+    # level) is wrong at every level and every pass replays
+    cls = rng.integers(0, 6, (45, 66))
+    mant = 1.0 + rng.integers(0, 128, (45, 66)) / 128.0
+    sign = np.where(rng.integers(0, 2, (45, 66)) == 1, -1.0, 1.0)
+    classes = sign * mant * np.exp2(-22.0 * cls)
     return {
+        "replay_every_level": classes,
         "uniform": S.make("uniform", 201, (130, 257), np.float64),
         "normal": S.make("normal", 202, (33, 70), np.float64),
         "wide": S.make("wide", 203, (70, 129), np.float64),
@@ -122,6 +130,18 @@ def test_split_f64_bit_exact(emu, case, as_b, mode):
     assert np.array_equal(vg, v), (vg, v)
     assert np.array_equal(got, ref)
     assert emu.domain_status() == st
+
+
+@pytest.mark.parametrize("nprod", [6, 21])
+def test_dgemm_replay_every_level_bit_exact(emu, nprod):
+    """(Deeper products of these classes fall below the FP32 range.)"""
+    X = _f64_cases()["replay_every_level"]
+    _, v, _, _ = O.split_f64(X)
+    assert all(v[r + 1] < v[r] - 9 for r in range(5))        # every level mis-speculated
+    A, B = X[:, :60], np.ascontiguousarray(X[:, 6:66].T)    # 45 x 60 and 60 x 45
+    ref, st = O.emu_dgemm(A, B, nprod)
+    C = emu.dgemm(dev(A), dev(np.ascontiguousarray(B)), nprod).cpu().numpy()
+    assert st == 0 and np.array_equal(C.view(np.uint64), ref.view(np.uint64))
 
 
 def test_split_f64_domain_flags(emu):
