@@ -204,15 +204,27 @@ __global__ __launch_bounds__(SPLIT_THREADS) void f64_maxabs_kernel(F64SplitArgs 
     double m = 0.0;
     unsigned flags = 0;
     const double lo = 0x1p-126, hi = 0x1.fep127;   // (2 - 2^-7) 2^127
+    // four independent loads in flight per thread (a row is read in steps of
+    // 4 x 256 consecutive entries)
+    constexpr int U = 4;
     for (int64_t r = b; r < op.rows; r += nb) {
         const double *row = op.X + r * op.ldx;
-        for (int64_t c = threadIdx.x; c < op.cols; c += SPLIT_THREADS) {
-            double x = row[c];
-            if (op.sc) x = ldexp(x, -op.sc[op.as_b ? c : r]);
-            const double ax = fabs(x);
-            if (!__builtin_isfinite(x)) { flags |= ST_NAN; continue; }
-            if (x != 0.0 && (ax < lo || ax > hi)) flags |= ST_RANGE;
-            if (ax > m) m = ax;
+        for (int64_t c0 = threadIdx.x; c0 < op.cols; c0 += U * SPLIT_THREADS) {
+            double x[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t c = c0 + u * SPLIT_THREADS;
+                x[u] = c < op.cols ? row[c] : 0.0;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t c = c0 + u * SPLIT_THREADS;
+                if (op.sc && c < op.cols) x[u] = ldexp(x[u], -op.sc[op.as_b ? c : r]);
+                const double ax = fabs(x[u]);
+                if (!__builtin_isfinite(x[u])) { flags |= ST_NAN; continue; }
+                if (x[u] != 0.0 && (ax < lo || ax > hi)) flags |= ST_RANGE;
+                if (ax > m) m = ax;
+            }
         }
     }
     for (int off = 32; off > 0; off >>= 1) m = fmax(m, __shfl_xor(m, off));
@@ -476,6 +488,16 @@ int grid_for_pairs(int64_t npairs) {
     return (int)(npairs < cap ? (npairs > 0 ? npairs : 1) : cap);
 }
 
+// Blocks of an FP64 split pass: about eight work items per block, between
+// 1024 and 4096 blocks per operand (fewer blocks also mean fewer atomics on
+// the per-level maxima at the end of each block; measured at N = 2048 and
+// 8192).
+int grid_for_pairs_f64(int64_t npairs) {
+    int64_t g = npairs / 8;
+    g = g < 1024 ? 1024 : (g > 4096 ? 4096 : g);
+    return (int)(npairs < g ? (npairs > 0 ? npairs : 1) : g);
+}
+
 }  // namespace
 
 // C = beta C (0 when beta == 0: C is then not read), the BLAS result when
@@ -538,12 +560,14 @@ hipError_t launch_split_f64(const F64SplitOperand *ops, int nops, int64_t KB, in
     a.KB = KB;
     a.status = status;
     f64_state_init<<<1, 64, 0, s>>>(a, nlev, mode);
-    auto max_blocks = [](int64_t rows) { return (int)(rows < 2048 ? (rows > 0 ? rows : 1) : 2048); };
+    // at most 512 blocks per operand: each ends in one atomic on the maximum
+    auto max_blocks = [](int64_t rows) { return (int)(rows < 512 ? (rows > 0 ? rows : 1) : 512); };
     a.blocks0 = max_blocks(ops[0].rows);
     const int gm = a.blocks0 + (nops > 1 ? max_blocks(ops[1].rows) : 0);
     f64_maxabs_kernel<<<gm, SPLIT_THREADS, 0, s>>>(a);
-    a.blocks0 = grid_for_pairs(KB * (ops[0].Rpad / ROWS_PER_BLOCK));
-    const int g = a.blocks0 + (nops > 1 ? grid_for_pairs(KB * (ops[1].Rpad / ROWS_PER_BLOCK)) : 0);
+    a.blocks0 = grid_for_pairs_f64(KB * (ops[0].Rpad / ROWS_PER_BLOCK));
+    const int g =
+        a.blocks0 + (nops > 1 ? grid_for_pairs_f64(KB * (ops[1].Rpad / ROWS_PER_BLOCK)) : 0);
     for (int pass = 0; pass < nlev; ++pass)
         split_f64_kernel<<<g, SPLIT_THREADS, 0, s>>>(a, pass);
     return hipGetLastError();
