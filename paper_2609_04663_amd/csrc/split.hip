@@ -271,11 +271,25 @@ __device__ __forceinline__ void split_f64_pass(const F64SplitOperand op, int64_t
         const int64_t k0 = ic.kb * KBLK + ic.q * 8;
         double x[8];
         const int wexp = (op.sc && ic.prow < prow_lim) ? -op.sc[ic.prow] : 0;   // weight 2^-s
+        const double *src = X + ic.prow * ldx + k0;
+        if (!AS_B && ic.prow < prow_lim && k0 + 8 <= k_lim &&
+            (reinterpret_cast<uintptr_t>(src) & 15u) == 0) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const bool ok = ic.prow < prow_lim && k0 + i < k_lim;
-            x[i] = ok ? (AS_B ? X[(k0 + i) * ldx + ic.prow] : X[ic.prow * ldx + k0 + i]) : 0.0;
-            if (op.sc) x[i] = ldexp(x[i], wexp);
+            for (int i = 0; i < 8; i += 2) {
+                const double2 t = *reinterpret_cast<const double2 *>(src + i);
+                x[i] = t.x;
+                x[i + 1] = t.y;
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const bool ok = ic.prow < prow_lim && k0 + i < k_lim;
+                x[i] = ok ? (AS_B ? X[(k0 + i) * ldx + ic.prow] : X[ic.prow * ldx + k0 + i]) : 0.0;
+            }
+        }
+        if (op.sc) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) x[i] = ldexp(x[i], wexp);
         }
         u16x8 outp[6];
 #pragma unroll
