@@ -126,7 +126,10 @@ int emu_dgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, doub
                  double *C, int64_t ldc, int nprod);
 
 /* Stream for subsequent calls (a hipStream_t); NULL selects the default
-   stream.  Always returns EMU_OK. */
+   stream.  Switching streams orders the new stream after the work already
+   queued on the previous one (an event dependency, no host synchronisation),
+   since every call uses the one workspace.  EMU_OK, or EMU_EHIP if the event
+   calls fail. */
 int emu_set_stream(void *hip_stream);
 
 /* Projection constant of the FP64 split for subsequent emu_dgemm and

@@ -17,6 +17,7 @@ namespace {
 using namespace emu;
 
 hipStream_t g_stream = nullptr;
+hipEvent_t g_switch_event = nullptr;   // orders a new stream after the previous one
 int g_split_mode = EMU_SPLIT_SYM;
 int g_split_scope = EMU_SCOPE_OPERAND;
 std::string g_err;
@@ -180,7 +181,23 @@ Shape plan(int64_t M, int64_t N, int64_t K, int nplanes, int tile_m, int tile_n)
 extern "C" {
 
 int emu_set_stream(void *hip_stream) {
-    g_stream = reinterpret_cast<hipStream_t>(hip_stream);
+    const hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+    if (s != g_stream && g_ws.base) {
+        // Every call shares the one workspace: work queued on the new stream
+        // must not start before the calls already queued on the old one are
+        // done with it.  An event dependency, no host synchronisation.
+        if (!g_switch_event) {
+            hipError_t e = hipEventCreateWithFlags(&g_switch_event, hipEventDisableTiming);
+            if (e != hipSuccess) {
+                g_switch_event = nullptr;
+                return hip_fail(e, "hipEventCreateWithFlags");
+            }
+        }
+        hipError_t e = hipEventRecord(g_switch_event, g_stream);
+        if (e == hipSuccess) e = hipStreamWaitEvent(s, g_switch_event, 0);
+        if (e != hipSuccess) return hip_fail(e, "stream switch");
+    }
+    g_stream = s;
     return EMU_OK;
 }
 
