@@ -300,9 +300,14 @@ int emu_sgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, floa
         return e == hipSuccess ? EMU_OK : hip_fail(e, "scale C");
     }
     const Shape s = plan(M, N, K, 3, SGEMM_MT, SGEMM_NT);
-    rc = ensure_workspace(s.bytesA + s.bytesB);
+    // few output tiles: split the reduction (partial sums after the planes)
+    const int splits = sgemm_splits(M, N, s.KB);
+    const size_t part_off = (s.bytesA + s.bytesB + 255) / 256 * 256;
+    const size_t part_bytes = splits > 1 ? (size_t)splits * M * N * sizeof(float) : 0;
+    rc = ensure_workspace(part_off + part_bytes);
     if (rc) return rc;
     uint16_t *Ap = ws_planes(0), *Bp = ws_planes(s.bytesA);
+    float *part = splits > 1 ? reinterpret_cast<float *>(ws_planes(part_off)) : nullptr;
     prof_mark(0);
     // op(A) rows are A's rows ('N') or A's columns ('T': A is K x M, packed as a
     // B operand); op(B) columns likewise; both operands in one launch
@@ -312,7 +317,8 @@ int emu_sgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, floa
     hipError_t e = launch_split_f32(ops, 2, s.KB, ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f32");
     prof_mark(1);
-    e = launch_gemm_f32(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, alpha, beta, g_stream);
+    e = launch_gemm_f32(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, alpha, beta, splits, part,
+                        g_stream);
     if (e != hipSuccess) return hip_fail(e, "gemm_f32");
     prof_mark(2);
     return EMU_OK;

@@ -114,9 +114,13 @@ hipError_t launch_unpack(const uint16_t *P, int nc, int64_t KB, int64_t Rpad, in
                          int64_t cols, bool as_b, uint16_t *out, hipStream_t s);
 hipError_t launch_copy_v(const F64SplitState *st, int32_t *v, hipStream_t s);
 // alpha, beta: C = alpha P + beta C (see out_update); 1, 0 stores P
+// Split-K factor of the emulated SGEMM: 1 unless the output tiles fill at most
+// half of the chip, else up to 16 splits of whole reduction panels.  splits > 1 needs part:
+// splits x M x N floats of scratch for the partial sums.
+int sgemm_splits(int64_t M, int64_t N, int64_t KB);
 hipError_t launch_gemm_f32(const uint16_t *Ap, const uint16_t *Bp, float *C, int64_t M, int64_t N,
                            int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc, float alpha,
-                           float beta, hipStream_t s);
+                           float beta, int splits, float *part, hipStream_t s);
 // sa, sb: row weights of A and column weights of B to restore (C_mn times
 // 2^(sa_m + sb_n)), or both null
 hipError_t launch_gemm_f64(const uint16_t *Ap, const uint16_t *Bp, double *C, int64_t M,

@@ -36,7 +36,7 @@ constexpr int B_CHUNKS = NC * B_BYTES / 1024;       // 24
 __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
     const uint16_t *__restrict__ Ap, const uint16_t *__restrict__ Bp, float *__restrict__ C,
     int64_t M, int64_t N, int KB, int64_t RpadA, int64_t RpadB, int64_t ldc, float alpha,
-    float beta, int nt_m, int nt_n) {
+    float beta, int nt_m, int nt_n, int kb_per_split, float *__restrict__ part) {
     __shared__ __attribute__((aligned(1024))) char stage0[STAGE];
     __shared__ __attribute__((aligned(1024))) char stage1[STAGE];
 
@@ -148,8 +148,11 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
     // copy of kb + 1 has landed; (3) starts the copy of kb + 2 into stage kb and
     // reads the sub-step-0 fragments of kb + 1 while the sub-step-1 MFMAs run.
     // The copy past the last k-block re-reads the last one (in bounds, unused).
-    static_for<COPIES>([&](auto j_c) { issue_one(0, stage0, j_c); });
-    static_for<COPIES>([&](auto j_c) { issue_one(min(1, KB - 1), stage1, j_c); });
+    // split-K: this workgroup reduces k-blocks [kb_lo, kb_hi), whole panels
+    const int kb_lo = blockIdx.y * kb_per_split;
+    const int kb_hi = min(KB, kb_lo + kb_per_split);
+    static_for<COPIES>([&](auto j_c) { issue_one(kb_lo, stage0, j_c); });
+    static_for<COPIES>([&](auto j_c) { issue_one(min(kb_lo + 1, kb_hi - 1), stage1, j_c); });
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(COPIES) : "memory");
     __syncthreads();
     Frags f;
@@ -163,10 +166,10 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
     }
     b0a[0] = f.b[0][0];
     b0a[1] = f.b[0][1];
-    int kb = 0;
+    int kb = kb_lo;
     f32x16 lo[RB][2];
-    for (int p0 = 0; p0 < KB; p0 += KB_PER_PANEL) {
-        const int p1 = min(KB, p0 + KB_PER_PANEL);
+    for (int p0 = kb_lo; p0 < kb_hi; p0 += KB_PER_PANEL) {
+        const int p1 = min(kb_hi, p0 + KB_PER_PANEL);
         f32x16 hi[RB][2];
         auto kblock = [&](auto first_c, auto first_lo_c) {
             char *cur = (kb & 1) ? stage1 : stage0;
@@ -177,10 +180,10 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
             asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
             pipeline_barrier();
             step(f, b0b, b0a, hi, lo, std::false_type{}, std::false_type{}, nxt, off0,
-                 min(kb + 2, KB - 1), cur, std::integral_constant<int, COPIES>{});
+                 min(kb + 2, kb_hi - 1), cur, std::integral_constant<int, COPIES>{});
             __builtin_amdgcn_sched_barrier(0);
         };
-        if (p0 == 0) kblock(std::true_type{}, std::true_type{});
+        if (p0 == kb_lo) kblock(std::true_type{}, std::true_type{});
         else kblock(std::true_type{}, std::false_type{});
         for (++kb; kb < p1; ++kb) kblock(std::false_type{}, std::false_type{});
 #pragma unroll
@@ -205,20 +208,62 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int64_t row = m0 + wm * 32 * RB + rb * 32 + acc_row(lane, r);
-                if (row < M && col < N)
-                    C[row * ldc + col] = out_update(blk[rb][cb][r], alpha, beta, C + row * ldc + col);
+                if (row < M && col < N) {
+                    if (part != nullptr)   // split-K: this split's sum, added by reduce_splits
+                        part[((int64_t)blockIdx.y * M + row) * N + col] = blk[rb][cb][r];
+                    else
+                        C[row * ldc + col] = out_update(blk[rb][cb][r], alpha, beta, C + row * ldc + col);
+                }
             }
         }
 }
 
+// Split-K combination: C = alpha (sum of the splits' partial sums, in split
+// order, FP32) + beta C, with the output update of the single-pass kernel.
+__global__ void reduce_splits_kernel(const float *__restrict__ part, int splits, int64_t M,
+                                     int64_t N, float *__restrict__ C, int64_t ldc, float alpha,
+                                     float beta) {
+    const int64_t total = M * N;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        float p = part[i];
+        for (int sp = 1; sp < splits; ++sp) p += part[sp * total + i];
+        const int64_t row = i / N, col = i - row * N;
+        C[row * ldc + col] = out_update(p, alpha, beta, C + row * ldc + col);
+    }
+}
+
 }  // namespace
+
+int sgemm_splits(int64_t M, int64_t N, int64_t KB) {
+    const int64_t tiles = ((M + MT - 1) / MT) * ((N + NT - 1) / NT);
+    const int64_t panels = (KB + KB_PER_PANEL - 1) / KB_PER_PANEL;
+    // split only when the tiles fill at most half of the 256 CUs, and keep all
+    // splits within one wave of workgroups (the partial sums cost a pass)
+    if (2 * tiles > 256 || panels < 2) return 1;
+    int64_t sp = 256 / tiles;
+    sp = sp < panels ? sp : panels;
+    sp = sp < 16 ? sp : 16;
+    const int64_t per = (panels + sp - 1) / sp;             // whole panels per split
+    return (int)((panels + per - 1) / per);
+}
 
 hipError_t launch_gemm_f32(const uint16_t *Ap, const uint16_t *Bp, float *C, int64_t M, int64_t N,
                            int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc, float alpha,
-                           float beta, hipStream_t s) {
+                           float beta, int splits, float *part, hipStream_t s) {
     const int nt_m = (int)((M + MT - 1) / MT), nt_n = (int)((N + NT - 1) / NT);
-    gemm_f32_kernel<<<nt_m * nt_n, 256, 0, s>>>(Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc, alpha,
-                                               beta, nt_m, nt_n);
+    const int64_t panels = (KB + KB_PER_PANEL - 1) / KB_PER_PANEL;
+    const int kb_per_split = (int)((panels + splits - 1) / splits) * KB_PER_PANEL;
+    if (splits < 1 || (splits > 1 && !part) || (int64_t)(splits - 1) * kb_per_split >= KB)
+        return hipErrorInvalidValue;
+    gemm_f32_kernel<<<dim3(nt_m * nt_n, splits), 256, 0, s>>>(
+        Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc, alpha, beta, nt_m, nt_n, kb_per_split,
+        splits > 1 ? part : nullptr);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || splits == 1) return e;
+    const int64_t total = M * N;
+    const int g = (int)((total + 255) / 256 < 8192 ? (total + 255) / 256 : 8192);
+    reduce_splits_kernel<<<g, 256, 0, s>>>(part, splits, M, N, C, ldc, alpha, beta);
     return hipGetLastError();
 }
 
