@@ -29,7 +29,7 @@ namespace {
 constexpr int MT = SGEMM_MT, NT = SGEMM_NT, NC = 3, RB = MT / 64;
 constexpr int A_BYTES = MT * 64;                    // one plane, one k-block
 constexpr int B_BYTES = NT * 64;
-constexpr int STAGE = NC * (A_BYTES + B_BYTES);     // 72 KB
+constexpr int STAGE = NC * (A_BYTES + B_BYTES);     // 60 KB
 constexpr int A_CHUNKS = NC * A_BYTES / 1024;       // 36
 constexpr int B_CHUNKS = NC * B_BYTES / 1024;       // 24
 
