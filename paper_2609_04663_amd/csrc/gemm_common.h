@@ -16,9 +16,10 @@ typedef __attribute__((address_space(3))) void *lds_void_ptr;
 // remap gives each XCD a contiguous run of tile ids, and tile ids walk the
 // output in groups of GROUP_M tile-rows so that the workgroups resident on one
 // XCD at a time share A row-panels and B column-panels in that XCD's L2.
+// Tile of virtual workgroup w out of nwg (a persistent workgroup w0 of a grid of
+// G, G a multiple of 8, takes w = w0, w0 + G, ...: the same XCD throughout).
 template <int GROUP_M>
-__device__ inline void tile_coords(int nt_m, int nt_n, int &tm, int &tn) {
-    const int nwg = gridDim.x, w = blockIdx.x;
+__device__ inline void tile_coords_of(int w, int nwg, int nt_m, int nt_n, int &tm, int &tn) {
     const int per = nwg / 8, rem = nwg % 8, x = w % 8, j = w / 8;
     const int id = (x < rem) ? x * (per + 1) + j : rem * (per + 1) + (x - rem) * per + j;
     const int group = GROUP_M * nt_n;
@@ -27,6 +28,10 @@ __device__ inline void tile_coords(int nt_m, int nt_n, int &tm, int &tn) {
     const int r = id - g * group;
     tm = first + r % gm;
     tn = r / gm;
+}
+template <int GROUP_M>
+__device__ inline void tile_coords(int nt_m, int nt_n, int &tm, int &tn) {
+    tile_coords_of<GROUP_M>(blockIdx.x, gridDim.x, nt_m, nt_n, tm, tn);
 }
 
 // One 1 KB direct global->LDS copy by a wave: lane l moves 16 bytes from

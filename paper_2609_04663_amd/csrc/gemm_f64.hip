@@ -357,20 +357,23 @@ __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
     const uint16_t *__restrict__ Ap, const uint16_t *__restrict__ Bp, double *__restrict__ C,
     int64_t M, int64_t N, int KB, int64_t RpadA, int64_t RpadB, int64_t ldc,
     const int *__restrict__ sa, const int *__restrict__ sb, double alpha, double beta, int nt_m,
-    int nt_n) {
+    int nt_n, int ntiles) {
     using K = CfgW<D, NS, ACC64_LDS>;
     __shared__ __attribute__((aligned(1024))) char lds[NS * K::STAGE + K::ACC64_BYTES];
     // lane-private FP64 accumulators in LDS: element e = 4 b + r of lane l of
     // wave w at (w * 8 + e) * 64 + l
     double *acc64_lds = reinterpret_cast<double *>(lds + NS * K::STAGE);
 
-    int tm, tn;
-    tile_coords<8>(nt_m, nt_n, tm, tn);
+    // Persistent workgroups: workgroup w0 of G takes tiles w0, w0 + G, ... (its
+    // `mine` tiles), walking one sequence of k-blocks tile after tile, so the
+    // copy ring runs on into the next tile's first k-blocks while a tile's
+    // FP64 epilogue and store execute.
+    const int G = gridDim.x;
+    const int mine = (ntiles - 1 - (int)blockIdx.x) / G + 1;
     const int lane = threadIdx.x & 63;
     const unsigned lane16 = (unsigned)lane * 16u;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wm = wave >> 1, wn = wave & 1;
-    const int64_t m0 = (int64_t)tm * K::MT, n0 = (int64_t)tn * K::NT;
 
     const char *Ag = reinterpret_cast<const char *>(Ap);
     const char *Bg = reinterpret_cast<const char *>(Bp);
@@ -379,20 +382,40 @@ __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
 
     // Copy c of a k-block by wave w: c < 3 moves 1 KB part (w & 1) of A plane
     // 2 c + (w >> 1); c >= 3 moves part w of B plane c - 3 (36 parts in all).
-    const int64_t a_src = m0 * 64 + (int64_t)(wave >> 1) * a_plane + (wave & 1) * 1024;
+    // ak, bk: the k-block's slab of plane 0 at the copied tile's first row.
+    const int64_t a_off = (int64_t)(wave >> 1) * a_plane + (wave & 1) * 1024;
     const int a_dst = (wave >> 1) * K::A_BYTES + (wave & 1) * 1024;
-    const int64_t b_src = n0 * 64 + (int64_t)wave * 1024;
+    const int64_t b_off = (int64_t)wave * 1024;
     const int b_dst = 6 * K::A_BYTES + wave * 1024;
-    auto issue_one = [&](int kb, char *base, auto c_c) {
+    auto issue_one = [&](const char *ak, const char *bk, char *base, auto c_c) {
         constexpr int c = decltype(c_c)::value;
         if constexpr (c < 3)
-            copy_1k(Ag + (int64_t)kb * RpadA * 64 + a_src + 2 * c * a_plane,
-                    base + a_dst + 2 * c * K::A_BYTES, lane16);
+            copy_1k(ak + a_off + 2 * c * a_plane, base + a_dst + 2 * c * K::A_BYTES, lane16);
         else
-            copy_1k(Bg + (int64_t)kb * RpadB * 64 + b_src + (c - 3) * b_plane,
-                    base + b_dst + (c - 3) * K::B_BYTES, lane16);
+            copy_1k(bk + b_off + (c - 3) * b_plane, base + b_dst + (c - 3) * K::B_BYTES, lane16);
     };
-    auto stage = [&](int kb) -> char * { return lds + (kb % NS) * K::STAGE; };
+    // Copy cursor: the (tile, k-block) the next copies fetch; past the last
+    // k-block of the last tile it stays on that k-block (in bounds, unused).
+    int c_tile = 0, c_kb = 0;
+    const char *c_ak, *c_bk;
+    auto cursor_bases = [&]() {
+        int tm, tn;
+        tile_coords_of<8>((int)blockIdx.x + c_tile * G, ntiles, nt_m, nt_n, tm, tn);
+        c_ak = Ag + (int64_t)c_kb * RpadA * 64 + (int64_t)tm * K::MT * 64;
+        c_bk = Bg + (int64_t)c_kb * RpadB * 64 + (int64_t)tn * K::NT * 64;
+    };
+    auto cursor_next = [&]() {
+        if (c_kb + 1 < KB) {
+            ++c_kb;
+            c_ak += RpadA * 64;
+            c_bk += RpadB * 64;
+        } else if (c_tile + 1 < mine) {
+            ++c_tile;
+            c_kb = 0;
+            cursor_bases();
+        }
+    };
+    auto stage = [&](int qs) -> char * { return lds + qs * K::STAGE; };
 
     // lane's fragment offset inside a 16-row block: row l % 16, chunk l / 16
     const int frow = lane & 15;
@@ -421,7 +444,7 @@ __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
     constexpr int CS = (SLOTS - 2) / K::COPIES;
     static_assert(RS * (K::READS - 1) < SLOTS && CS >= 1, "slots");
     auto trip = [&](const Frags &cur, f32x4 (&acc)[K::P][2], auto zero_c, int nso, Frags &nxt,
-                    int ckb, char *cdst) {
+                    const char *ak, const char *bk, char *cdst) {
         constexpr bool zero = decltype(zero_c)::value;
         static_for<SLOTS>([&](auto t_c) {
             constexpr int t = decltype(t_c)::value;
@@ -437,87 +460,119 @@ __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
                 read_one(nso, nxt, std::integral_constant<int, t / RS>{});
             order_fence();
             if constexpr (t >= 2 && (t - 2) % CS == 0 && (t - 2) / CS < K::COPIES)
-                issue_one(ckb, cdst, std::integral_constant<int, (t - 2) / CS>{});
+                issue_one(ak, bk, cdst, std::integral_constant<int, (t - 2) / CS>{});
             order_fence();
         });
     };
 
-    double acc64[2][4];
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            acc64[b][r] = 0.0;
-            if constexpr (ACC64_LDS) acc64_lds[(wave * 8 + 4 * b + r) * 64 + lane] = 0.0;
-        }
-
-    // Ring of NS stages, k-block kb in stage kb mod NS.  Trip kb starts once
-    // every wave's copies of k-block kb + 1 have landed and every wave has read
-    // k-block kb into registers (one barrier); it then runs the MFMAs of kb,
-    // reads kb + 1 and issues the copies of kb + NS into the stage of kb.
-    // Copies past the last k-block re-read it (in bounds, never used).
-    for (int j = 0; j < NS; ++j)
-        static_for<K::COPIES>([&](auto c_c) { issue_one(min(j, KB - 1), stage(j), c_c); });
+    // Ring of NS stages; the k-block at position q of the workgroup's sequence
+    // sits in stage q mod NS.  Trip q starts once every wave's copies of q + 1
+    // have landed and every wave has read q into registers (one barrier); it
+    // then runs the MFMAs of q, reads q + 1 and issues the copies of q + NS into
+    // the stage of q.  Across a tile boundary q + 1 is the next tile's first
+    // k-block, already in place, so only the first tile waits for a fill.
+    cursor_bases();
+    for (int j = 0; j < NS; ++j) {
+        static_for<K::COPIES>([&](auto c_c) { issue_one(c_ak, c_bk, stage(j), c_c); });
+        cursor_next();
+    }
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NS - 1) * K::COPIES) : "memory");
     __syncthreads();
     Frags f0, f1;
     static_for<K::READS>([&](auto t_c) { read_one(0, f0, t_c); });
-    int kb = 0;
+    int qs = 0;                        // q mod NS
     auto one = [&](const Frags &cur, Frags &nxt, f32x4 (&acc)[K::P][2], auto zero_c) {
         asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"((NS - 2) * K::COPIES) : "memory");
         pipeline_barrier();
-        trip(cur, acc, zero_c, ((kb + 1) % NS) * K::STAGE, nxt, min(kb + NS, KB - 1), stage(kb));
+        const int qn = qs + 1 == NS ? 0 : qs + 1;
+        trip(cur, acc, zero_c, qn * K::STAGE, nxt, c_ak, c_bk, stage(qs));
         __builtin_amdgcn_sched_barrier(0);
-        ++kb;
+        cursor_next();
+        qs = qn;
     };
-    for (int p0 = 0; p0 < KB; p0 += KB_PER_PANEL) {
-        const int p1 = min(KB, p0 + KB_PER_PANEL);
-        f32x4 acc[K::P][2];
-        // trips alternate the fragment buffers; a panel starts on f0 (its
-        // length is even unless it is the last one)
-        one(f0, f1, acc, std::true_type{});
-        while (kb < p1) {
-            one(f1, f0, acc, std::false_type{});
-            if (kb < p1) one(f0, f1, acc, std::false_type{});
-        }
-        // panel end: widen each product exactly and add it in FP64, in order
-#pragma unroll
-        for (int q = K::Q_VGPR; q < K::P; ++q)
-#pragma unroll
-            for (int b = 0; b < 2; ++b) mfma16_vacc_settle(acc[q][b]);
-        // eight independent FP64 chains, products in order
-        if constexpr (ACC64_LDS) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) acc64[e / 4][e % 4] = acc64_lds[(wave * 8 + e) * 64 + lane];
-        }
-#pragma unroll
-        for (int q = 0; q < K::P; ++q)
-#pragma unroll
-            for (int b = 0; b < 2; ++b)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) acc64[b][r] += (double)acc[q][b][r];
-        if constexpr (ACC64_LDS) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) acc64_lds[(wave * 8 + e) * 64 + lane] = acc64[e / 4][e % 4];
-        }
-    }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
-    const int64_t row0 = m0 + wm * 16 + (lane >> 4) * 4;
+    for (int it = 0; it < mine; ++it) {
+        int tm, tn;
+        tile_coords_of<8>((int)blockIdx.x + it * G, ntiles, nt_m, nt_n, tm, tn);
+        const int64_t m0 = (int64_t)tm * K::MT, n0 = (int64_t)tn * K::NT;
+        double acc64[2][4];
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-        const int64_t col = n0 + wn * 32 + b * 16 + (lane & 15);
-        const int col_w = (sa != nullptr && col < N) ? sb[col] : 0;
+        for (int b = 0; b < 2; ++b)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int64_t row = row0 + r;
-            if (row < M && col < N) {
-                double val = acc64[b][r];
-                if (sa != nullptr) val = ldexp(val, sa[row] + col_w);
-                C[row * ldc + col] = out_update(val, alpha, beta, C + row * ldc + col);
+            for (int r = 0; r < 4; ++r) {
+                acc64[b][r] = 0.0;
+                if constexpr (ACC64_LDS) acc64_lds[(wave * 8 + 4 * b + r) * 64 + lane] = 0.0;
+            }
+        // trips alternate the fragment buffers: a panel starts on f0 (panels
+        // have even length, except the last panel of a tile when KB is odd,
+        // and then the workgroup has one tile)
+        for (int p0 = 0; p0 < KB; p0 += KB_PER_PANEL) {
+            const int p1 = min(KB, p0 + KB_PER_PANEL);
+            f32x4 acc[K::P][2];
+            int kb = p0;
+            one(f0, f1, acc, std::true_type{});
+            for (++kb; kb < p1; ++kb) {
+                one(f1, f0, acc, std::false_type{});
+                if (++kb < p1) one(f0, f1, acc, std::false_type{});
+            }
+            // panel end: widen each product exactly and add it in FP64, in order
+#pragma unroll
+            for (int q = K::Q_VGPR; q < K::P; ++q)
+#pragma unroll
+                for (int b = 0; b < 2; ++b) mfma16_vacc_settle(acc[q][b]);
+            // eight independent FP64 chains, products in order
+            if constexpr (ACC64_LDS) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    acc64[e / 4][e % 4] = acc64_lds[(wave * 8 + e) * 64 + lane];
+            }
+#pragma unroll
+            for (int q = 0; q < K::P; ++q)
+#pragma unroll
+                for (int b = 0; b < 2; ++b)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) acc64[b][r] += (double)acc[q][b][r];
+            if constexpr (ACC64_LDS) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    acc64_lds[(wave * 8 + e) * 64 + lane] = acc64[e / 4][e % 4];
+            }
+        }
+
+        const int64_t row0 = m0 + wm * 16 + (lane >> 4) * 4;
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            const int64_t col = n0 + wn * 32 + b * 16 + (lane & 15);
+            const int col_w = (sa != nullptr && col < N) ? sb[col] : 0;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int64_t row = row0 + r;
+                if (row < M && col < N) {
+                    double val = acc64[b][r];
+                    if (sa != nullptr) val = ldexp(val, sa[row] + col_w);
+                    C[row * ldc + col] = out_update(val, alpha, beta, C + row * ldc + col);
+                }
             }
         }
     }
+    // the last trips issued (unused) copies: let them land before the workgroup
+    // ends and its LDS is handed to another workgroup
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+// Persistent grid of the d >= 6 kernel: one workgroup per CU (its LDS use
+// allows one), rounded down to a multiple of 8.
+int persistent_workgroups() {
+    static int g = 0;
+    if (g == 0) {
+        int dev = 0, cus = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            cus < 8)
+            cus = 256;
+        g = cus / 8 * 8;
+    }
+    return g;
 }
 
 template <int D, int NS, bool ACC64_LDS>
@@ -526,8 +581,19 @@ hipError_t launch_w(const uint16_t *Ap, const uint16_t *Bp, double *C, int64_t M
                     const int *sb, double alpha, double beta, hipStream_t s) {
     using K = CfgW<D, NS, ACC64_LDS>;
     const int nt_m = (int)((M + K::MT - 1) / K::MT), nt_n = (int)((N + K::NT - 1) / K::NT);
-    gemm_f64w_kernel<D, NS, ACC64_LDS><<<nt_m * nt_n, 256, 0, s>>>(Ap, Bp, C, M, N, (int)KB, RpadA, RpadB,
-                                                         ldc, sa, sb, alpha, beta, nt_m, nt_n);
+    const int ntiles = nt_m * nt_n;
+    // Short reductions (K <= 1024): one persistent workgroup per CU (a
+    // multiple of 8: every workgroup keeps its XCD), so the next tile's first
+    // copies overlap a tile's epilogue and store (measured at 16384^2 x 512,
+    // d = 6: 17 % less time).  Longer reductions: one workgroup per tile
+    // (persistent was 4-9 % slower at K = 8192).  With an odd number of
+    // k-blocks a second tile would start on the other fragment buffer, so
+    // those always take one tile per workgroup.
+    const int pw = persistent_workgroups();
+    const int G = (KB % 2 == 0 && KB <= 32 && ntiles > pw) ? pw : ntiles;
+    gemm_f64w_kernel<D, NS, ACC64_LDS><<<G, 256, 0, s>>>(Ap, Bp, C, M, N, (int)KB, RpadA, RpadB,
+                                                         ldc, sa, sb, alpha, beta, nt_m, nt_n,
+                                                         ntiles);
     return hipGetLastError();
 }
 

@@ -130,3 +130,23 @@ def test_dgemm_rowcol_depths_bit_exact(emu, nprod):
     finally:
         emu.set_split_scope(emu.SCOPE_OPERAND)
     assert same_bits(C, ref)
+
+
+@pytest.mark.parametrize("K", [640, 600])
+@pytest.mark.parametrize("nprod", [21, 36])
+def test_dgemm_persistent_tiles_bit_exact(emu, K, nprod):
+    """More output tiles than CUs and a short reduction: the d >= 6 kernel runs
+    persistent workgroups that walk several tiles each, the copy ring running
+    on across tile boundaries (even k-block count, K = 640), or one tile per
+    workgroup (odd, K = 600).  Sampled entries, including the last tile row and
+    column."""
+    M = N = 1100
+    A = S.make("wide", 961, (M, K), np.float64)
+    B = S.make("uniform", 962, (K, N), np.float64)
+    C = emu.dgemm(dev(A), dev(B), nprod).cpu().numpy()
+    rng = np.random.default_rng(K + nprod)
+    r = np.concatenate([[0, M - 1, 0, M - 1, M - 5], rng.integers(0, M, 379)]).astype(np.int64)
+    c = np.concatenate([[0, 0, N - 1, N - 1, N - 7], rng.integers(0, N, 379)]).astype(np.int64)
+    ref, st = O.emu_dgemm_entries(A, B, r, c, nprod)
+    assert st == 0
+    assert same_bits(np.ascontiguousarray(C[r, c]), ref)
