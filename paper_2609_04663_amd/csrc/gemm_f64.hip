@@ -90,25 +90,28 @@ constexpr int read_code(int t) {
     return -1;
 }
 
-template <int D, int BM, int NS, bool ACC64_LDS, int AFTER>
+template <int D, int BM, int NS, bool ACC64_LDS, int AFTER, bool PERSIST>
 __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
     const uint16_t *__restrict__ Ap, const uint16_t *__restrict__ Bp, double *__restrict__ C,
     int64_t M, int64_t N, int KB, int64_t RpadA, int64_t RpadB, int64_t ldc,
     const int *__restrict__ sa, const int *__restrict__ sb, double alpha, double beta, int nt_m,
-    int nt_n) {
+    int nt_n, int ntiles) {
     using K = Cfg<D, BM, NS, ACC64_LDS, AFTER>;
+    static_assert(K::COPIES_AFTER == K::COPIES, "one k-block's copies per trip (cursor below)");
     __shared__ __attribute__((aligned(1024))) char lds[K::NSTAGE * K::STAGE + K::ACC64_BYTES];
     // lane-private FP64 accumulators in LDS: element r of lane l of wave w at
     // ((w * BM + b) * 16 + r) * 64 + l (consecutive lanes, consecutive doubles)
     double *acc64_lds = reinterpret_cast<double *>(lds + K::NSTAGE * K::STAGE);
 
-    int tm, tn;
-    tile_coords<8>(nt_m, nt_n, tm, tn);
+    // PERSIST: workgroup w0 of G takes tiles w0, w0 + G, ... (`mine` of them)
+    // and walks them as one sequence of k-blocks, the copies running on into
+    // the next tile; otherwise one tile per workgroup.
+    const int G = gridDim.x;
+    const int mine = PERSIST ? (ntiles - 1 - (int)blockIdx.x) / G + 1 : 1;
     const int lane = threadIdx.x & 63;
     const unsigned lane16 = (unsigned)lane * 16u;   // copy offset of this lane
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
     const int wm = wave >> 1, wn = wave & 1;
-    const int64_t m0 = (int64_t)tm * K::MT, n0 = (int64_t)tn * K::NT;
 
     const char *Ag = reinterpret_cast<const char *>(Ap);
     const char *Bg = reinterpret_cast<const char *>(Bp);
@@ -117,26 +120,43 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
 
     // Copy issue for one k-block: wave w moves 1 KB parts [w BM, (w + 1) BM) of
     // every A plane and part w of every B plane (wave-uniform base plus
-    // compile-time offsets).
-    const int64_t a_base = m0 * 64 + (int64_t)wave * BM * 1024;
-    const int64_t b_base = n0 * 64 + (int64_t)wave * 1024;
+    // compile-time offsets).  ak, bk: the k-block's slab of plane 0 at the
+    // copied tile's first row.
+    const int64_t a_base = (int64_t)wave * BM * 1024;
+    const int64_t b_base = (int64_t)wave * 1024;
     // Copy j of a k-block (j < COPIES) moves plane c = j / (BM + 1), A part
     // j % (BM + 1) (or the B part when that is BM).
-    auto issue_one = [&](int kb, char *base, auto j_c) {
+    auto issue_one = [&](const char *ak, const char *bk, char *base, auto j_c) {
         constexpr int j = decltype(j_c)::value, c = j / (BM + 1), r = j % (BM + 1);
         if constexpr (r < BM)
-            copy_1k(Ag + (int64_t)kb * RpadA * 64 + a_base + c * a_plane + r * 1024,
+            copy_1k(ak + a_base + c * a_plane + r * 1024,
                     base + wave * BM * 1024 + c * K::A_BYTES + r * 1024, lane16);
         else
-            copy_1k(Bg + (int64_t)kb * RpadB * 64 + b_base + c * b_plane,
-                    base + D * K::A_BYTES + wave * 1024 + c * K::B_BYTES, lane16);
+            copy_1k(bk + b_base + c * b_plane, base + D * K::A_BYTES + wave * 1024 + c * K::B_BYTES,
+                    lane16);
     };
-    auto issue_all = [&](int kb, char *base) {
-        static_for<K::COPIES>([&](auto j_c) { issue_one(kb, base, j_c); });
+    // Copy cursor: the (tile, k-block) the next copies fetch; past the last
+    // k-block of the last tile it stays on that k-block (in bounds, unused).
+    int c_tile = 0, c_kb = 0;
+    const char *c_ak, *c_bk;
+    auto cursor_bases = [&]() {
+        int tm, tn;
+        tile_coords_of<8>((int)blockIdx.x + c_tile * G, ntiles, nt_m, nt_n, tm, tn);
+        c_ak = Ag + (int64_t)c_kb * RpadA * 64 + (int64_t)tm * K::MT * 64;
+        c_bk = Bg + (int64_t)c_kb * RpadB * 64 + (int64_t)tn * K::NT * 64;
     };
-    // copies issued after the mid-k-block barrier; the rest go out before it
-    constexpr int H0 = K::COPIES_AFTER;
-    auto stage = [&](int kb) -> char * { return lds + (kb % K::NSTAGE) * K::STAGE; };
+    auto cursor_next = [&]() {
+        if (c_kb + 1 < KB) {
+            ++c_kb;
+            c_ak += RpadA * 64;
+            c_bk += RpadB * 64;
+        } else if (PERSIST && c_tile + 1 < mine) {
+            ++c_tile;
+            c_kb = 0;
+            cursor_bases();
+        }
+    };
+    auto stage = [&](int qs) -> char * { return lds + qs * K::STAGE; };
 
     const int off0 = frag_offset(lane, 0), off1 = frag_offset(lane, 1);
 
@@ -164,7 +184,7 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
     // not matter (exact panel sums).
     constexpr int SLOTS = K::MMAS > K::READS ? K::MMAS : K::READS;
     auto step = [&](const Frags &cur, f32x16 (&acc)[K::P][BM], auto zero_c, int nso, int noff,
-                    Frags &nxt, int ckb, char *cdst, auto j0_c, auto j1_c) {
+                    Frags &nxt, const char *ak, const char *bk, char *cdst, auto j0_c, auto j1_c) {
         constexpr bool zero = decltype(zero_c)::value;
         constexpr int J0 = decltype(j0_c)::value, J1 = decltype(j1_c)::value;
         static_for<(SLOTS > J1 - J0 ? SLOTS : J1 - J0)>([&](auto t_c) {
@@ -188,120 +208,128 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
                     nxt.a[plane][blk] = lds_frag(At0 + nso + plane * K::A_BYTES + blk * 32 * 64, noff);
             }
             order_fence();
-            if constexpr (t < J1 - J0) issue_one(ckb, cdst, std::integral_constant<int, J0 + t>{});
+            if constexpr (t < J1 - J0)
+                issue_one(ak, bk, cdst, std::integral_constant<int, J0 + t>{});
             order_fence();
         });
     };
 
-    double acc64[ACC64_LDS ? 1 : BM][16];
-#pragma unroll
-    for (int b = 0; b < BM; ++b)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            if constexpr (ACC64_LDS)
-                acc64_lds[((wave * BM + b) * 16 + r) * 64 + lane] = 0.0;
-            else
-                acc64[b][r] = 0.0;
-        }
-
-    // Software pipeline over k-blocks with a ring of NS LDS stages (stage of
-    // k-block kb: kb mod NS).  The copy of k-block kb + NS goes to stage kb,
-    // which is free once trip kb's mid barrier has passed: its first H0 copies
-    // are issued right after that barrier, the rest in trip kb + 1 before its
-    // barrier.  Trip kb (1) reads the sub-step-1 fragments of kb while the
-    // sub-step-0 MFMAs run, and issues the remaining copies of k-block
-    // kb + NS - 1; (2) waits until at most the newest NS - 2 k-blocks of its own
-    // copies are outstanding (so kb + 1 has landed) and for its LDS reads, then
-    // barriers: every wave is done reading stage kb and every copy of kb + 1 has
-    // landed; (3) issues the first H0 copies of k-block kb + NS into stage kb and
-    // reads the sub-step-0 fragments of kb + 1 while the sub-step-1 MFMAs run.
-    // Copies past the last k-block re-read the last one (in bounds, never used).
-    for (int j = 0; j < K::NSTAGE - 1; ++j) issue_all(min(j, KB - 1), stage(j));
-    static_for<H0>([&](auto j_c) { issue_one(min(K::NSTAGE - 1, KB - 1), stage(K::NSTAGE - 1), j_c); });
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((K::NSTAGE - 2) * K::COPIES + H0) : "memory");
+    // Software pipeline over the workgroup's sequence of k-blocks with a ring of
+    // NS LDS stages (position q in stage q mod NS).  Trip q (1) reads the
+    // sub-step-1 fragments of q while the sub-step-0 MFMAs run; (2) waits until
+    // at most the newest NS - 2 k-blocks of its own copies are outstanding (so
+    // q + 1 has landed) and for its LDS reads, then barriers: every wave is done
+    // reading stage q and every copy of q + 1 has landed; (3) issues the copies
+    // of q + NS into stage q and reads the sub-step-0 fragments of q + 1 while
+    // the sub-step-1 MFMAs run.  Across a tile boundary q + 1 is the next tile's
+    // first k-block, already in place.
+    cursor_bases();
+    for (int j = 0; j < K::NSTAGE; ++j) {
+        static_for<K::COPIES>([&](auto j_c) { issue_one(c_ak, c_bk, stage(j), j_c); });
+        cursor_next();
+    }
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((K::NSTAGE - 2) * K::COPIES + K::COPIES) : "memory");
     __syncthreads();
     Frags f0, f1;
     load(0, off0, f0);
-    int kb = 0;
-    for (int p0 = 0; p0 < KB; p0 += KB_PER_PANEL) {
-        const int p1 = min(KB, p0 + KB_PER_PANEL);
-        f32x16 acc[K::P][BM];
-        auto kblock = [&](auto first_c) {
-            const int so = (kb % K::NSTAGE) * K::STAGE;
-            const int nso = ((kb + 1) % K::NSTAGE) * K::STAGE;
-            // sub-step 0 of kb; reads sub-step 1 of kb
-            step(f0, acc, first_c, so, off1, f1, min(kb + K::NSTAGE - 1, KB - 1),
-                 stage(kb + K::NSTAGE - 1), std::integral_constant<int, H0>{},
-                 std::integral_constant<int, K::COPIES>{});
-            __builtin_amdgcn_sched_barrier(0);
-            if constexpr (K::NSTAGE == 2)
-                asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
-            else
-                asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"((K::NSTAGE - 2) * K::COPIES)
-                             : "memory");
-            pipeline_barrier();
-            // sub-step 1 of kb; reads sub-step 0 of kb + 1
-            step(f1, acc, std::false_type{}, nso, off0, f0, min(kb + K::NSTAGE, KB - 1), lds + so,
-                 std::integral_constant<int, 0>{}, std::integral_constant<int, H0>{});
-            __builtin_amdgcn_sched_barrier(0);
-        };
-        kblock(std::true_type{});
-        for (++kb; kb < p1; ++kb) kblock(std::false_type{});
-        // panel end: widen each product exactly and add it in FP64, in order
+    int qs = 0;                        // q mod NS
+    auto kblock = [&](f32x16 (&acc)[K::P][BM], auto first_c) {
+        const int so = qs * K::STAGE;
+        const int qn = qs + 1 == K::NSTAGE ? 0 : qs + 1;
+        // sub-step 0 of q; reads sub-step 1 of q
+        step(f0, acc, first_c, so, off1, f1, c_ak, c_bk, stage(qs),
+             std::integral_constant<int, K::COPIES>{}, std::integral_constant<int, K::COPIES>{});
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (K::NSTAGE == 2)
+            asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+        else
+            asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"((K::NSTAGE - 2) * K::COPIES)
+                         : "memory");
+        pipeline_barrier();
+        // sub-step 1 of q; reads sub-step 0 of q + 1; copies of q + NS into stage q
+        step(f1, acc, std::false_type{}, qn * K::STAGE, off0, f0, c_ak, c_bk, stage(qs),
+             std::integral_constant<int, 0>{}, std::integral_constant<int, K::COPIES>{});
+        __builtin_amdgcn_sched_barrier(0);
+        cursor_next();
+        qs = qn;
+    };
+
+    for (int it = 0; it < mine; ++it) {
+        int tm, tn;
+        tile_coords_of<8>((int)blockIdx.x + it * G, ntiles, nt_m, nt_n, tm, tn);
+        const int64_t m0 = (int64_t)tm * K::MT, n0 = (int64_t)tn * K::NT;
+        double acc64[ACC64_LDS ? 1 : BM][16];
 #pragma unroll
-        for (int q = K::Q_VGPR; q < K::P; ++q)
+        for (int b = 0; b < BM; ++b)
 #pragma unroll
-            for (int b = 0; b < BM; ++b) mfma_vacc_settle(acc[q][b]);
-        if constexpr (ACC64_LDS) {
-            // eight elements at a time: eight independent FP64 chains keep the
-            // FP64 adder busy (one element's 21 adds in a row would wait on
-            // each other)
+            for (int r = 0; r < 16; ++r) {
+                if constexpr (ACC64_LDS)
+                    acc64_lds[((wave * BM + b) * 16 + r) * 64 + lane] = 0.0;
+                else
+                    acc64[b][r] = 0.0;
+            }
+        for (int p0 = 0; p0 < KB; p0 += KB_PER_PANEL) {
+            const int p1 = min(KB, p0 + KB_PER_PANEL);
+            f32x16 acc[K::P][BM];
+            kblock(acc, std::true_type{});
+            for (int kb = p0 + 1; kb < p1; ++kb) kblock(acc, std::false_type{});
+            // panel end: widen each product exactly and add it in FP64, in order
 #pragma unroll
-            for (int b = 0; b < BM; ++b)
+            for (int q = K::Q_VGPR; q < K::P; ++q)
 #pragma unroll
-                for (int h = 0; h < 16; h += 8) {
-                    double t[8];
-#pragma unroll
-                    for (int r = 0; r < 8; ++r)
-                        t[r] = acc64_lds[((wave * BM + b) * 16 + h + r) * 64 + lane];
-#pragma unroll
-                    for (int q = 0; q < K::P; ++q)
-#pragma unroll
-                        for (int r = 0; r < 8; ++r) t[r] += (double)acc[q][b][h + r];
-#pragma unroll
-                    for (int r = 0; r < 8; ++r)
-                        acc64_lds[((wave * BM + b) * 16 + h + r) * 64 + lane] = t[r];
-                }
-        } else {
-#pragma unroll
-            for (int q = 0; q < K::P; ++q)
+                for (int b = 0; b < BM; ++b) mfma_vacc_settle(acc[q][b]);
+            if constexpr (ACC64_LDS) {
+                // eight elements at a time: eight independent FP64 chains keep
+                // the FP64 adder busy (one element's 21 adds in a row would wait
+                // on each other)
 #pragma unroll
                 for (int b = 0; b < BM; ++b)
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) acc64[b][r] += (double)acc[q][b][r];
+                    for (int h = 0; h < 16; h += 8) {
+                        double t[8];
+#pragma unroll
+                        for (int r = 0; r < 8; ++r)
+                            t[r] = acc64_lds[((wave * BM + b) * 16 + h + r) * 64 + lane];
+#pragma unroll
+                        for (int q = 0; q < K::P; ++q)
+#pragma unroll
+                            for (int r = 0; r < 8; ++r) t[r] += (double)acc[q][b][h + r];
+#pragma unroll
+                        for (int r = 0; r < 8; ++r)
+                            acc64_lds[((wave * BM + b) * 16 + h + r) * 64 + lane] = t[r];
+                    }
+            } else {
+#pragma unroll
+                for (int q = 0; q < K::P; ++q)
+#pragma unroll
+                    for (int b = 0; b < BM; ++b)
+#pragma unroll
+                        for (int r = 0; r < 16; ++r) acc64[b][r] += (double)acc[q][b][r];
+            }
+        }
+
+        // store; with the scale-aware split the row and column weights go back
+        // in here, C_mn = 2^(sa_m + sb_n) C'_mn (exact up to overflow or underflow)
+        const int col_w =
+            (sa != nullptr && n0 + wn * 32 + (lane & 31) < N) ? sb[n0 + wn * 32 + (lane & 31)] : 0;
+#pragma unroll
+        for (int b = 0; b < BM; ++b) {
+            const int64_t col = n0 + wn * 32 + (lane & 31);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int64_t row = m0 + wm * 32 * BM + b * 32 + acc_row(lane, r);
+                if (row < M && col < N) {
+                    double val = ACC64_LDS ? acc64_lds[((wave * BM + b) * 16 + r) * 64 + lane]
+                                           : acc64[ACC64_LDS ? 0 : b][r];
+                    if (sa != nullptr) val = ldexp(val, sa[row] + col_w);
+                    C[row * ldc + col] = out_update(val, alpha, beta, C + row * ldc + col);
+                }
+            }
         }
     }
     // the last trips issued (unused) copies: let them land before the workgroup
     // ends and its LDS is handed to another workgroup
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-
-    // store; with the scale-aware split the row and column weights go back in
-    // here, C_mn = 2^(sa_m + sb_n) C'_mn (exact up to overflow or underflow)
-    const int col_w = (sa != nullptr && n0 + wn * 32 + (lane & 31) < N) ? sb[n0 + wn * 32 + (lane & 31)] : 0;
-#pragma unroll
-    for (int b = 0; b < BM; ++b) {
-        const int64_t col = n0 + wn * 32 + (lane & 31);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int64_t row = m0 + wm * 32 * BM + b * 32 + acc_row(lane, r);
-            if (row < M && col < N) {
-                double val = ACC64_LDS ? acc64_lds[((wave * BM + b) * 16 + r) * 64 + lane]
-                                       : acc64[ACC64_LDS ? 0 : b][r];
-                if (sa != nullptr) val = ldexp(val, sa[row] + col_w);
-                C[row * ldc + col] = out_update(val, alpha, beta, C + row * ldc + col);
-            }
-        }
-    }
 }
 
 // ---------------------------------------------------------------------------
@@ -352,7 +380,7 @@ constexpr int read_code_w(int t) {
     return -1;
 }
 
-template <int D, int NS, bool ACC64_LDS>
+template <int D, int NS, bool ACC64_LDS, bool PERSIST>
 __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
     const uint16_t *__restrict__ Ap, const uint16_t *__restrict__ Bp, double *__restrict__ C,
     int64_t M, int64_t N, int KB, int64_t RpadA, int64_t RpadB, int64_t ldc,
@@ -369,7 +397,7 @@ __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
     // copy ring runs on into the next tile's first k-blocks while a tile's
     // FP64 epilogue and store execute.
     const int G = gridDim.x;
-    const int mine = (ntiles - 1 - (int)blockIdx.x) / G + 1;
+    const int mine = PERSIST ? (ntiles - 1 - (int)blockIdx.x) / G + 1 : 1;
     const int lane = threadIdx.x & 63;
     const unsigned lane16 = (unsigned)lane * 16u;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -409,7 +437,7 @@ __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
             ++c_kb;
             c_ak += RpadA * 64;
             c_bk += RpadB * 64;
-        } else if (c_tile + 1 < mine) {
+        } else if (PERSIST && c_tile + 1 < mine) {
             ++c_tile;
             c_kb = 0;
             cursor_bases();
@@ -560,7 +588,7 @@ __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
-// Persistent grid of the d >= 6 kernel: one workgroup per CU (its LDS use
+// Persistent grid of the DGEMM kernels: one workgroup per CU (their LDS use
 // allows one), rounded down to a multiple of 8.
 int persistent_workgroups() {
     static int g = 0;
@@ -586,14 +614,17 @@ hipError_t launch_w(const uint16_t *Ap, const uint16_t *Bp, double *C, int64_t M
     // multiple of 8: every workgroup keeps its XCD), so the next tile's first
     // copies overlap a tile's epilogue and store (measured at 16384^2 x 512,
     // d = 6: 17 % less time).  Longer reductions: one workgroup per tile
-    // (persistent was 4-9 % slower at K = 8192).  With an odd number of
+    // (persistent was 4-9 % slower at K = 8192; a separate instantiation keeps
+    // their kernel free of the tile-walking code).  With an odd number of
     // k-blocks a second tile would start on the other fragment buffer, so
     // those always take one tile per workgroup.
     const int pw = persistent_workgroups();
-    const int G = (KB % 2 == 0 && KB <= 32 && ntiles > pw) ? pw : ntiles;
-    gemm_f64w_kernel<D, NS, ACC64_LDS><<<G, 256, 0, s>>>(Ap, Bp, C, M, N, (int)KB, RpadA, RpadB,
-                                                         ldc, sa, sb, alpha, beta, nt_m, nt_n,
-                                                         ntiles);
+    if (KB % 2 == 0 && KB <= 32 && ntiles > pw)
+        gemm_f64w_kernel<D, NS, ACC64_LDS, true><<<pw, 256, 0, s>>>(
+            Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, nt_m, nt_n, ntiles);
+    else
+        gemm_f64w_kernel<D, NS, ACC64_LDS, false><<<ntiles, 256, 0, s>>>(
+            Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, nt_m, nt_n, ntiles);
     return hipGetLastError();
 }
 
@@ -603,8 +634,18 @@ hipError_t launch_t(const uint16_t *Ap, const uint16_t *Bp, double *C, int64_t M
                     const int *sb, double alpha, double beta, hipStream_t s) {
     using K = Cfg<D, BM, NS, ACC64_LDS, AFTER>;
     const int nt_m = (int)((M + K::MT - 1) / K::MT), nt_n = (int)((N + K::NT - 1) / K::NT);
-    gemm_f64_kernel<D, BM, NS, ACC64_LDS, AFTER><<<nt_m * nt_n, 256, 0, s>>>(Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc,
-                                                       sa, sb, alpha, beta, nt_m, nt_n);
+    const int ntiles = nt_m * nt_n;
+    // short reductions: persistent workgroups (as in launch_w; every k-block
+    // starts on f0, so any number of k-blocks works).  A separate
+    // instantiation, so that the one-tile kernel of long reductions carries
+    // none of the tile-walking code (it cost up to 7 % at 8192 for d = 5).
+    const int pw = persistent_workgroups();
+    if (KB <= 32 && ntiles > pw)
+        gemm_f64_kernel<D, BM, NS, ACC64_LDS, AFTER, true><<<pw, 256, 0, s>>>(
+            Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, nt_m, nt_n, ntiles);
+    else
+        gemm_f64_kernel<D, BM, NS, ACC64_LDS, AFTER, false><<<ntiles, 256, 0, s>>>(
+            Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, nt_m, nt_n, ntiles);
     return hipGetLastError();
 }
 

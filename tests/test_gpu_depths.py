@@ -133,13 +133,14 @@ def test_dgemm_rowcol_depths_bit_exact(emu, nprod):
 
 
 @pytest.mark.parametrize("K", [640, 600])
-@pytest.mark.parametrize("nprod", [21, 36])
+@pytest.mark.parametrize("nprod", [10, 15, 21, 36])
 def test_dgemm_persistent_tiles_bit_exact(emu, K, nprod):
-    """More output tiles than CUs and a short reduction: the d >= 6 kernel runs
+    """More output tiles than CUs and a short reduction: both DGEMM kernels run
     persistent workgroups that walk several tiles each, the copy ring running
-    on across tile boundaries (even k-block count, K = 640), or one tile per
-    workgroup (odd, K = 600).  Sampled entries, including the last tile row and
-    column."""
+    on across tile boundaries.  The d >= 6 kernel needs an even k-block count
+    (K = 640) and takes one tile per workgroup otherwise (K = 600); the d <= 5
+    kernel (nprod 10, 15: 324 tiles of 64 x 64) takes either.  Sampled entries,
+    including the last tile row and column."""
     M = N = 1100
     A = S.make("wide", 961, (M, K), np.float64)
     B = S.make("uniform", 962, (K, N), np.float64)
