@@ -151,3 +151,20 @@ def test_dgemm_persistent_tiles_bit_exact(emu, K, nprod):
     ref, st = O.emu_dgemm_entries(A, B, r, c, nprod)
     assert st == 0
     assert same_bits(np.ascontiguousarray(C[r, c]), ref)
+
+
+@pytest.mark.parametrize("nprod", [1, 3, 6])
+def test_dgemm_persistent_large_tiles_bit_exact(emu, nprod):
+    """The persistent d <= 5 kernel with its larger tiles (256 x 64 for nprod 1,
+    128 x 64 for 3 and 6): 2100 x 2100 outputs give more tiles than CUs."""
+    M = N = 2100
+    K = 640
+    A = S.make("normal", 971, (M, K), np.float64)
+    B = S.make("wide", 972, (K, N), np.float64)
+    C = emu.dgemm(dev(A), dev(B), nprod).cpu().numpy()
+    rng = np.random.default_rng(nprod)
+    r = np.concatenate([[0, M - 1, 0, M - 1], rng.integers(0, M, 380)]).astype(np.int64)
+    c = np.concatenate([[0, 0, N - 1, N - 1], rng.integers(0, N, 380)]).astype(np.int64)
+    ref, st = O.emu_dgemm_entries(A, B, r, c, nprod)
+    assert st == 0
+    assert same_bits(np.ascontiguousarray(C[r, c]), ref)
