@@ -12,9 +12,12 @@
 // depends only on the order of the FP64 additions, which here is the paper's:
 // panel ascending, diagonal l = i + j ascending, i ascending inside a diagonal.
 //
-// Two kernels.  Depths d <= 5 (below): 32 x 32 x 16 MFMA, 4 waves in a 2 x 2
-// grid; wave tile (32 BM) x 32, output tile (64 BM) x 64.  Depths d >= 6
-// (gemm_f64w_kernel further down): 16 x 16 x 32 MFMA on a 16 x 32 wave tile.  Per k-block of 32 the d planes of both operands are copied
+// Two kernels.  gemm_f64_kernel (below): 32 x 32 x 16 MFMA, 4 waves in a 2 x 2
+// grid; wave tile (32 BM) x 32, output tile (64 BM) x 64.  gemm_f64w_kernel
+// (further down): 16 x 16 x 32 MFMA on a (16 BMW) x 32 wave tile, one barrier
+// per k-block; it runs depths d >= 6 (BMW = 1) and, with BMW = 2, the long
+// reductions of d = 2 and 5 and the small grids of d = 1 .. 3 (the choice is
+// made in launch_gemm_f64).  Per k-block of 32 the d planes of both operands are copied
 // straight into LDS (global_load_lds_dwordx4) through a ring of LDS stages.
 // Each wave keeps one FP32 accumulator set per product for the whole panel
 // (all N_p live, so every fragment read from LDS feeds every product that
@@ -336,41 +339,49 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
 // Depths d = 6 .. 11 (21 .. 36 products, every slice of both operands).  For
 // d >= 7 a 32 x 32 wave tile would need 16 N_p accumulator registers per lane,
 // more than the register file holds, so these depths use the 16 x 16 x 32 MFMA
-// on a 16 x 32 wave tile (two 16 x 16 blocks along N): 8 registers per
-// product.  Workgroup: 4 waves in a 2 x 2 grid, output tile 32 x 64; one
+// on a 16 x 32 wave tile (BMW = 1: two 16 x 16 blocks along N): 8 registers
+// per product.  Workgroup: 4 waves in a 2 x 2 grid, output tile 32 x 64; one
 // k-block of 32 reduction indices (one MFMA depth) per trip and one barrier
 // per trip, with the copies and fragment reads spread over the trip's MFMAs
 // and copies issued two trips ahead.  d = 6 runs here too: measured at
 // M = N = K = 8192 it is about 5 % faster than on the 32 x 32 kernel.
-template <int D, int NS, bool ACC64_LDS>
+// Depths d <= 5 (d planes per operand) can take a 32 x 32 wave tile here
+// (BMW = 2: 2 x 2 blocks, 16 registers per product, output tile 64 x 64).
+template <int D, int NS, bool ACC64_LDS, int BMW>
 struct CfgW {
     static constexpr int P = n_prod(D);
-    // FP64 accumulator tile in LDS (8 doubles per lane) instead of VGPRs
-    static constexpr int ACC64_BYTES = ACC64_LDS ? 4 * 64 * 8 * 8 : 0;
-    static constexpr int MT = 32, NT = 64;
+    static constexpr int NPL = D < 6 ? D : 6;                        // slices read per operand
+    // FP64 accumulator tile in LDS (8 BMW doubles per lane) instead of VGPRs
+    static constexpr int ACC64_BYTES = ACC64_LDS ? 4 * 64 * 8 * BMW * 8 : 0;
+    static constexpr int MT = 32 * BMW, NT = 64;                     // wave tile 16 BMW x 32
     static constexpr int A_BYTES = MT * 64, B_BYTES = NT * 64;       // one plane of a stage
-    static constexpr int STAGE = 6 * (A_BYTES + B_BYTES);
+    static constexpr int STAGE = NPL * (A_BYTES + B_BYTES);
     static constexpr int COPIES = STAGE / 1024 / 4;                  // 1 KB copies per wave
-    static constexpr int READS = 6 * 3;                              // A: 6 planes, B: 6 x 2 blocks
-    static constexpr int MMAS = 2 * P;
-    // AGPRs hold 32 products x 2 blocks x 4 registers; later products use VGPRs
-    static constexpr int Q_VGPR = P > 32 ? 32 : P;
-    static_assert(COPIES == 9 && 4 * COPIES * 1024 == STAGE, "copy split");
+    static constexpr int A_COPIES = NPL * MT / 16 / 4;               // the first ones move A
+    static constexpr int READS = NPL * (BMW + 2);                    // A: BMW blocks, B: 2
+    static constexpr int MMAS = 2 * BMW * P;
+    // AGPRs hold 32 / BMW products of 2 BMW blocks; later products use VGPRs
+    static constexpr int Q_VGPR = P > 32 / BMW ? 32 / BMW : P;
+    static_assert(BMW == 1 || BMW == 2, "wave tile");
+    static_assert(4 * COPIES * 1024 == STAGE && 4 * A_COPIES * 1024 == NPL * A_BYTES,
+                  "copy split");
+    static_assert(BMW == 2 || NPL == 6, "one-block tiles copy six planes");
     static_assert(NS * STAGE + ACC64_BYTES <= 160 * 1024, "LDS");
 };
 
 // Read t of a trip loads the t-th distinct fragment in order of first use by
 // the trip's MFMA sequence (product q on block b for MFMA 2 q + b), encoded as
 // 64 * is_B + 8 * plane + block.
-template <int D>
+template <int D, int BMW>
 constexpr int read_code_w(int t) {
-    bool seen_a[6] = {}, seen_b[6][2] = {};
+    bool seen_a[6][2] = {}, seen_b[6][2] = {};
     int r = 0;
-    for (int u = 0; u < 2 * n_prod(D); ++u) {
-        const int q = u / 2, b = u % 2, i = prod_i(q), j = prod_j(q);
-        if (!seen_a[i]) {
-            seen_a[i] = true;
-            if (r++ == t) return 8 * i;
+    for (int u = 0; u < 2 * BMW * n_prod(D); ++u) {
+        const int q = u / (2 * BMW), a = (u % (2 * BMW)) / 2, b = u % 2, i = prod_i(q),
+                  j = prod_j(q);
+        if (!seen_a[i][a]) {
+            seen_a[i][a] = true;
+            if (r++ == t) return 8 * i + a;
         }
         if (!seen_b[j][b]) {
             seen_b[j][b] = true;
@@ -380,16 +391,16 @@ constexpr int read_code_w(int t) {
     return -1;
 }
 
-template <int D, int NS, bool ACC64_LDS, bool PERSIST>
+template <int D, int NS, bool ACC64_LDS, bool PERSIST, int BMW>
 __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
     const uint16_t *__restrict__ Ap, const uint16_t *__restrict__ Bp, double *__restrict__ C,
     int64_t M, int64_t N, int KB, int64_t RpadA, int64_t RpadB, int64_t ldc,
     const int *__restrict__ sa, const int *__restrict__ sb, double alpha, double beta, int nt_m,
     int nt_n, int ntiles) {
-    using K = CfgW<D, NS, ACC64_LDS>;
+    using K = CfgW<D, NS, ACC64_LDS, BMW>;
     __shared__ __attribute__((aligned(1024))) char lds[NS * K::STAGE + K::ACC64_BYTES];
-    // lane-private FP64 accumulators in LDS: element e = 4 b + r of lane l of
-    // wave w at (w * 8 + e) * 64 + l
+    // lane-private FP64 accumulators in LDS: element e = 4 (2 a + b) + r of
+    // lane l of wave w at (w * 8 BMW + e) * 64 + l
     double *acc64_lds = reinterpret_cast<double *>(lds + NS * K::STAGE);
 
     // Persistent workgroups: workgroup w0 of G takes tiles w0, w0 + G, ... (its
@@ -408,19 +419,25 @@ __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
     const int64_t a_plane = (int64_t)KB * RpadA * 64;
     const int64_t b_plane = (int64_t)KB * RpadB * 64;
 
-    // Copy c of a k-block by wave w: c < 3 moves 1 KB part (w & 1) of A plane
-    // 2 c + (w >> 1); c >= 3 moves part w of B plane c - 3 (36 parts in all).
+    // Copy c of a k-block by wave w moves 1 KB part g = 4 c + w of the list
+    // A parts (plane-major), then B parts: for BMW = 1, c < 3 moves part
+    // (w & 1) of A plane 2 c + (w >> 1); for BMW = 2, c < NPL moves part w of
+    // A plane c; the rest move part w of B plane c - A_COPIES.
     // ak, bk: the k-block's slab of plane 0 at the copied tile's first row.
-    const int64_t a_off = (int64_t)(wave >> 1) * a_plane + (wave & 1) * 1024;
-    const int a_dst = (wave >> 1) * K::A_BYTES + (wave & 1) * 1024;
+    const int64_t a_off = BMW == 1 ? (int64_t)(wave >> 1) * a_plane + (wave & 1) * 1024
+                                   : (int64_t)wave * 1024;
+    const int a_dst = BMW == 1 ? (wave >> 1) * K::A_BYTES + (wave & 1) * 1024 : wave * 1024;
+    constexpr int A_STEP = BMW == 1 ? 2 : 1;             // A planes per copy index
     const int64_t b_off = (int64_t)wave * 1024;
-    const int b_dst = 6 * K::A_BYTES + wave * 1024;
+    const int b_dst = K::NPL * K::A_BYTES + wave * 1024;
     auto issue_one = [&](const char *ak, const char *bk, char *base, auto c_c) {
         constexpr int c = decltype(c_c)::value;
-        if constexpr (c < 3)
-            copy_1k(ak + a_off + 2 * c * a_plane, base + a_dst + 2 * c * K::A_BYTES, lane16);
+        if constexpr (c < K::A_COPIES)
+            copy_1k(ak + a_off + A_STEP * c * a_plane, base + a_dst + A_STEP * c * K::A_BYTES,
+                    lane16);
         else
-            copy_1k(bk + b_off + (c - 3) * b_plane, base + b_dst + (c - 3) * K::B_BYTES, lane16);
+            copy_1k(bk + b_off + (c - K::A_COPIES) * b_plane,
+                    base + b_dst + (c - K::A_COPIES) * K::B_BYTES, lane16);
     };
     // Copy cursor: the (tile, k-block) the next copies fetch; past the last
     // k-block of the last tile it stays on that k-block (in bounds, unused).
@@ -448,20 +465,21 @@ __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
     // lane's fragment offset inside a 16-row block: row l % 16, chunk l / 16
     const int frow = lane & 15;
     const int foff = frow * 64 + (((lane >> 4) ^ swz(frow)) << 4);
-    const char *const At0 = lds + (wm * 16) * 64 + foff;
-    const char *const Bt0 = lds + 6 * K::A_BYTES + (wn * 32) * 64 + foff;
+    const char *const At0 = lds + (wm * 16 * BMW) * 64 + foff;
+    const char *const Bt0 = lds + K::NPL * K::A_BYTES + (wn * 32) * 64 + foff;
 
     struct Frags {
-        bf16x8 a[6], b[6][2];
+        bf16x8 a[K::NPL][BMW], b[K::NPL][2];
     };
     auto read_one = [&](int so, Frags &f, auto t_c) {
-        constexpr int code = read_code_w<D>(decltype(t_c)::value);
+        constexpr int code = read_code_w<D, BMW>(decltype(t_c)::value);
         constexpr int plane = (code >> 3) & 7, blk = code & 7;
         if constexpr (code >= 64)
             f.b[plane][blk] =
                 *reinterpret_cast<const bf16x8 *>(Bt0 + so + plane * K::B_BYTES + blk * 16 * 64);
         else
-            f.a[plane] = *reinterpret_cast<const bf16x8 *>(At0 + so + plane * K::A_BYTES);
+            f.a[plane][blk] =
+                *reinterpret_cast<const bf16x8 *>(At0 + so + plane * K::A_BYTES + blk * 16 * 64);
     };
 
     // One trip: the MMAS MFMAs on `cur`; read t of the next k-block (stage
@@ -471,17 +489,19 @@ __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
     constexpr int RS = SLOTS >= 2 * K::READS ? 2 : 1;
     constexpr int CS = (SLOTS - 2) / K::COPIES;
     static_assert(RS * (K::READS - 1) < SLOTS && CS >= 1, "slots");
-    auto trip = [&](const Frags &cur, f32x4 (&acc)[K::P][2], auto zero_c, int nso, Frags &nxt,
-                    const char *ak, const char *bk, char *cdst) {
+    auto trip = [&](const Frags &cur, f32x4 (&acc)[K::P][2 * BMW], auto zero_c, int nso,
+                    Frags &nxt, const char *ak, const char *bk, char *cdst) {
         constexpr bool zero = decltype(zero_c)::value;
         static_for<SLOTS>([&](auto t_c) {
             constexpr int t = decltype(t_c)::value;
-            constexpr int q = t / 2, b = t % 2, i = prod_i(q), j = prod_j(q);
+            // product q on block e = 2 a + b (A block a, B block b)
+            constexpr int q = t / (2 * BMW), e = t % (2 * BMW), a = e / 2, b = e % 2;
+            constexpr int i = prod_i(q), j = prod_j(q);
             if constexpr (q >= K::Q_VGPR) {
-                if constexpr (zero) mfma16_vacc_zero(acc[q][b], cur.a[i], cur.b[j][b]);
-                else mfma16_vacc(acc[q][b], cur.a[i], cur.b[j][b]);
+                if constexpr (zero) mfma16_vacc_zero(acc[q][e], cur.a[i][a], cur.b[j][b]);
+                else mfma16_vacc(acc[q][e], cur.a[i][a], cur.b[j][b]);
             } else {
-                acc[q][b] = mfma16(cur.a[i], cur.b[j][b], zero ? f32x4{} : acc[q][b]);
+                acc[q][e] = mfma16(cur.a[i][a], cur.b[j][b], zero ? f32x4{} : acc[q][e]);
             }
             order_fence();
             if constexpr (t % RS == 0 && t / RS < K::READS)
@@ -509,7 +529,7 @@ __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
     Frags f0, f1;
     static_for<K::READS>([&](auto t_c) { read_one(0, f0, t_c); });
     int qs = 0;                        // q mod NS
-    auto one = [&](const Frags &cur, Frags &nxt, f32x4 (&acc)[K::P][2], auto zero_c) {
+    auto one = [&](const Frags &cur, Frags &nxt, f32x4 (&acc)[K::P][2 * BMW], auto zero_c) {
         asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"((NS - 2) * K::COPIES) : "memory");
         pipeline_barrier();
         const int qn = qs + 1 == NS ? 0 : qs + 1;
@@ -523,20 +543,21 @@ __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
         int tm, tn;
         tile_coords_of<8>((int)blockIdx.x + it * G, ntiles, nt_m, nt_n, tm, tn);
         const int64_t m0 = (int64_t)tm * K::MT, n0 = (int64_t)tn * K::NT;
-        double acc64[2][4];
+        double acc64[2 * BMW][4];
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int e = 0; e < 2 * BMW; ++e)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                acc64[b][r] = 0.0;
-                if constexpr (ACC64_LDS) acc64_lds[(wave * 8 + 4 * b + r) * 64 + lane] = 0.0;
+                acc64[e][r] = 0.0;
+                if constexpr (ACC64_LDS)
+                    acc64_lds[(wave * 8 * BMW + 4 * e + r) * 64 + lane] = 0.0;
             }
         // trips alternate the fragment buffers: a panel starts on f0 (panels
         // have even length, except the last panel of a tile when KB is odd,
         // and then the workgroup has one tile)
         for (int p0 = 0; p0 < KB; p0 += KB_PER_PANEL) {
             const int p1 = min(KB, p0 + KB_PER_PANEL);
-            f32x4 acc[K::P][2];
+            f32x4 acc[K::P][2 * BMW];
             int kb = p0;
             one(f0, f1, acc, std::true_type{});
             for (++kb; kb < p1; ++kb) {
@@ -547,36 +568,37 @@ __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
 #pragma unroll
             for (int q = K::Q_VGPR; q < K::P; ++q)
 #pragma unroll
-                for (int b = 0; b < 2; ++b) mfma16_vacc_settle(acc[q][b]);
-            // eight independent FP64 chains, products in order
+                for (int e = 0; e < 2 * BMW; ++e) mfma16_vacc_settle(acc[q][e]);
+            // 8 BMW independent FP64 chains, products in order
             if constexpr (ACC64_LDS) {
 #pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    acc64[e / 4][e % 4] = acc64_lds[(wave * 8 + e) * 64 + lane];
+                for (int x = 0; x < 8 * BMW; ++x)
+                    acc64[x / 4][x % 4] = acc64_lds[(wave * 8 * BMW + x) * 64 + lane];
             }
 #pragma unroll
             for (int q = 0; q < K::P; ++q)
 #pragma unroll
-                for (int b = 0; b < 2; ++b)
+                for (int e = 0; e < 2 * BMW; ++e)
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) acc64[b][r] += (double)acc[q][b][r];
+                    for (int r = 0; r < 4; ++r) acc64[e][r] += (double)acc[q][e][r];
             if constexpr (ACC64_LDS) {
 #pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    acc64_lds[(wave * 8 + e) * 64 + lane] = acc64[e / 4][e % 4];
+                for (int x = 0; x < 8 * BMW; ++x)
+                    acc64_lds[(wave * 8 * BMW + x) * 64 + lane] = acc64[x / 4][x % 4];
             }
         }
 
-        const int64_t row0 = m0 + wm * 16 + (lane >> 4) * 4;
 #pragma unroll
-        for (int b = 0; b < 2; ++b) {
+        for (int e = 0; e < 2 * BMW; ++e) {
+            const int a = e / 2, b = e % 2;
+            const int64_t row0 = m0 + wm * 16 * BMW + a * 16 + (lane >> 4) * 4;
             const int64_t col = n0 + wn * 32 + b * 16 + (lane & 15);
             const int col_w = (sa != nullptr && col < N) ? sb[col] : 0;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int64_t row = row0 + r;
                 if (row < M && col < N) {
-                    double val = acc64[b][r];
+                    double val = acc64[e][r];
                     if (sa != nullptr) val = ldexp(val, sa[row] + col_w);
                     C[row * ldc + col] = out_update(val, alpha, beta, C + row * ldc + col);
                 }
@@ -603,11 +625,13 @@ int persistent_workgroups() {
     return g;
 }
 
-template <int D, int NS, bool ACC64_LDS>
+// PERSIST_OK = false: the caller only launches long reductions here, which
+// never take the persistent grid (its instantiation is then not built).
+template <int D, int NS, bool ACC64_LDS, int BMW = 1, bool PERSIST_OK = true>
 hipError_t launch_w(const uint16_t *Ap, const uint16_t *Bp, double *C, int64_t M, int64_t N,
                     int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc, const int *sa,
                     const int *sb, double alpha, double beta, hipStream_t s) {
-    using K = CfgW<D, NS, ACC64_LDS>;
+    using K = CfgW<D, NS, ACC64_LDS, BMW>;
     const int nt_m = (int)((M + K::MT - 1) / K::MT), nt_n = (int)((N + K::NT - 1) / K::NT);
     const int ntiles = nt_m * nt_n;
     // Short reductions (K <= 1024): one persistent workgroup per CU (a
@@ -619,12 +643,16 @@ hipError_t launch_w(const uint16_t *Ap, const uint16_t *Bp, double *C, int64_t M
     // k-blocks a second tile would start on the other fragment buffer, so
     // those always take one tile per workgroup.
     const int pw = persistent_workgroups();
-    if (KB % 2 == 0 && KB <= 32 && ntiles > pw)
-        gemm_f64w_kernel<D, NS, ACC64_LDS, true><<<pw, 256, 0, s>>>(
-            Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, nt_m, nt_n, ntiles);
-    else
-        gemm_f64w_kernel<D, NS, ACC64_LDS, false><<<ntiles, 256, 0, s>>>(
-            Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, nt_m, nt_n, ntiles);
+    if constexpr (PERSIST_OK) {
+        if (KB % 2 == 0 && KB <= 32 && ntiles > pw) {
+            gemm_f64w_kernel<D, NS, ACC64_LDS, true, BMW><<<pw, 256, 0, s>>>(
+                Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, nt_m, nt_n,
+                ntiles);
+            return hipGetLastError();
+        }
+    }
+    gemm_f64w_kernel<D, NS, ACC64_LDS, false, BMW><<<ntiles, 256, 0, s>>>(
+        Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, nt_m, nt_n, ntiles);
     return hipGetLastError();
 }
 
@@ -655,12 +683,35 @@ hipError_t launch_gemm_f64(const uint16_t *Ap, const uint16_t *Bp, double *C, in
                            int64_t N, int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc,
                            const int *sa, const int *sb, double alpha, double beta, int d,
                            hipStream_t s) {
+    // Depths 1 .. 5 take the wide kernel's 64 x 64 tiles (BMW = 2) where it
+    // measured faster than the 32 x 32 x 16 kernel: long reductions (K > 1024)
+    // of d = 2 (8 % at 8192^3) and d = 5 (5 %), and grids of d = 1 .. 3 whose
+    // 128- or 256-row tiles would number fewer than the CUs (1.5 - 1.9x at
+    // 1000 x 1000 x 8200).  d = 4, and the large grids of d = 1 and 3, measured
+    // faster on the 32 x 32 x 16 kernel.  Both kernels give the same bits.
+    const int pw = persistent_workgroups();
+    auto few_tiles = [&](int64_t mt) {
+        return ((M + mt - 1) / mt) * ((N + DGEMM_NT - 1) / DGEMM_NT) < pw;
+    };
+    const bool long_k = KB > 32;
     switch (d) {
-        case 1: return launch_t<1, 4, 4, false, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
-        case 2: return launch_t<2, 2, 4, false, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
-        case 3: return launch_t<3, 2, 3, false, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
+        case 1:
+            if (few_tiles(256))
+                return launch_w<1, 4, false, 2>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
+            return launch_t<1, 4, 4, false, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
+        case 2:
+            if (long_k || few_tiles(128))
+                return launch_w<2, 4, false, 2>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
+            return launch_t<2, 2, 4, false, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
+        case 3:
+            if (few_tiles(128))
+                return launch_w<3, 4, false, 2>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
+            return launch_t<3, 2, 3, false, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
         case 4: return launch_t<4, 1, 3, false, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
-        case 5: return launch_t<5, 1, 3, true, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
+        case 5:
+            if (long_k)
+                return launch_w<5, 3, true, 2, false>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
+            return launch_t<5, 1, 3, true, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
         case 6: return launch_w<6, 4, false>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
         case 7: return launch_w<7, 3, false>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
         case 8: return launch_w<8, 3, true>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);

@@ -1,7 +1,7 @@
 """GPU parity at every depth of the triangular product selection,
-Eq. (product-selection): nprod = N_p(d) for d = 1, 2 (the existing multi-product
-kernel with one or three products) and d = 7 .. 11 (26 .. 36 products, the
-16 x 16 x 32 MFMA kernel).  The bar is the same as for the paper's depths:
+Eq. (product-selection): nprod = N_p(d) for d = 1, 2 (one or three products)
+and d = 7 .. 11 (26 .. 36 products, the 16 x 16 x 32 MFMA kernel), and the
+choice between the two DGEMM kernels that depths 1 .. 5 make by shape.  The bar is the same as for the paper's depths:
 bit-exact against the oracle (every panel product is an exact FP32 value and
 both sides add them in the same FP64 order).  Inputs are seeded and synthetic;
 the shapes span several tiles of every kernel with ragged tails."""
@@ -155,7 +155,7 @@ def test_dgemm_persistent_tiles_bit_exact(emu, K, nprod):
 
 @pytest.mark.parametrize("nprod", [1, 3, 6])
 def test_dgemm_persistent_large_tiles_bit_exact(emu, nprod):
-    """The persistent d <= 5 kernel with its larger tiles (256 x 64 for nprod 1,
+    """The persistent 32 x 32 x 16 kernel with its larger tiles (256 x 64 for nprod 1,
     128 x 64 for 3 and 6): 2100 x 2100 outputs give more tiles than CUs."""
     M = N = 2100
     K = 640
@@ -165,6 +165,41 @@ def test_dgemm_persistent_large_tiles_bit_exact(emu, nprod):
     rng = np.random.default_rng(nprod)
     r = np.concatenate([[0, M - 1, 0, M - 1], rng.integers(0, M, 380)]).astype(np.int64)
     c = np.concatenate([[0, 0, N - 1, N - 1], rng.integers(0, N, 380)]).astype(np.int64)
+    ref, st = O.emu_dgemm_entries(A, B, r, c, nprod)
+    assert st == 0
+    assert same_bits(np.ascontiguousarray(C[r, c]), ref)
+
+
+# (M, N, K, nprod, kernel the shape selects).  "32x32": the 32 x 32 x 16
+# kernel; "wide": the 16 x 16 x 32 kernel with 64 x 64 tiles; "persistent":
+# its persistent grid (more 64 x 64 tiles than CUs, an even number of
+# k-blocks of 32, K <= 1024).  Depths 1 and 3 take the wide kernel when their
+# 256- or 128-row tiles number fewer than 256; depth 2 also for K > 1024;
+# depth 5 only for K > 1024.
+ROUTES = [
+    (2100, 1900, 1500, 1, "32x32"),       # 270 tiles of 256 x 64, 47 k-blocks
+    (1000, 1000, 1100, 1, "wide"),        # 64 tiles of 256 x 64, 35 k-blocks
+    (1500, 1000, 640, 3, "persistent"),   # 192 tiles of 128 x 64 -> 384 of 64 x 64
+    (700, 600, 1100, 3, "wide"),          # long reduction
+    (2100, 1900, 1500, 6, "32x32"),       # 510 tiles of 128 x 64
+    (1000, 900, 1100, 6, "wide"),         # 120 tiles of 128 x 64
+    (1500, 1000, 640, 6, "persistent"),
+    (700, 600, 1100, 15, "wide"),         # long reduction, odd k-block count
+    (700, 600, 1000, 15, "32x32"),        # K <= 1024
+]
+
+
+@pytest.mark.parametrize("M,N,K,nprod,kernel", ROUTES)
+def test_dgemm_kernel_routes_bit_exact(emu, M, N, K, nprod, kernel):
+    """Each kernel that depths 1 .. 5 can select, at ragged shapes: sampled
+    entries, including the corners of the last tile row and column, are
+    bit-identical to the oracle's."""
+    A = S.make("wide", 981 + nprod, (M, K), np.float64)
+    B = S.make("normal", 982 + nprod, (K, N), np.float64)
+    C = emu.dgemm(dev(A), dev(B), nprod).cpu().numpy()
+    rng = np.random.default_rng(M + K + nprod)
+    r = np.concatenate([[0, M - 1, 0, M - 1, M - 3], rng.integers(0, M, 251)]).astype(np.int64)
+    c = np.concatenate([[0, 0, N - 1, N - 1, N - 5], rng.integers(0, N, 251)]).astype(np.int64)
     ref, st = O.emu_dgemm_entries(A, B, r, c, nprod)
     assert st == 0
     assert same_bits(np.ascontiguousarray(C[r, c]), ref)
