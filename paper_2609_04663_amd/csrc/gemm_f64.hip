@@ -16,7 +16,7 @@
 // grid; wave tile (32 BM) x 32, output tile (64 BM) x 64.  gemm_f64w_kernel
 // (further down): 16 x 16 x 32 MFMA on a (16 BMW) x 32 wave tile, one barrier
 // per k-block; it runs depths d >= 6 (BMW = 1) and, with BMW = 2, the long
-// reductions of d = 2 and 5 and the small grids of d = 1 .. 3 (the choice is
+// reductions of d = 2, 4, 5 and the small grids of d = 1 .. 3 (the choice is
 // made in launch_gemm_f64).  Per k-block of 32 the d planes of both operands are copied
 // straight into LDS (global_load_lds_dwordx4) through a ring of LDS stages.
 // Each wave keeps one FP32 accumulator set per product for the whole panel
@@ -685,10 +685,11 @@ hipError_t launch_gemm_f64(const uint16_t *Ap, const uint16_t *Bp, double *C, in
                            hipStream_t s) {
     // Depths 1 .. 5 take the wide kernel's 64 x 64 tiles (BMW = 2) where it
     // measured faster than the 32 x 32 x 16 kernel: long reductions (K > 1024)
-    // of d = 2 (8 % at 8192^3) and d = 5 (5 %), and grids of d = 1 .. 3 whose
-    // 128- or 256-row tiles would number fewer than the CUs (1.5 - 1.9x at
-    // 1000 x 1000 x 8200).  d = 4, and the large grids of d = 1 and 3, measured
-    // faster on the 32 x 32 x 16 kernel.  Both kernels give the same bits.
+    // of d = 2, 4 and 5 (8, 2 and 5 % at 8192^3), and grids of d = 1 .. 3
+    // whose 128- or 256-row tiles would number fewer than the CUs (1.5 - 1.9x
+    // at 1000 x 1000 x 8200).  Short reductions of d = 2, 4, 5 and the large
+    // grids of d = 1 and 3 measured faster on the 32 x 32 x 16 kernel.  Both
+    // kernels give the same bits.
     const int pw = persistent_workgroups();
     auto few_tiles = [&](int64_t mt) {
         return ((M + mt - 1) / mt) * ((N + DGEMM_NT - 1) / DGEMM_NT) < pw;
@@ -707,7 +708,10 @@ hipError_t launch_gemm_f64(const uint16_t *Ap, const uint16_t *Bp, double *C, in
             if (few_tiles(128))
                 return launch_w<3, 4, false, 2>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
             return launch_t<3, 2, 3, false, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
-        case 4: return launch_t<4, 1, 3, false, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
+        case 4:
+            if (long_k)
+                return launch_w<4, 4, false, 2, false>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
+            return launch_t<4, 1, 3, false, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
         case 5:
             if (long_k)
                 return launch_w<5, 3, true, 2, false>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);

@@ -175,7 +175,7 @@ def test_dgemm_persistent_large_tiles_bit_exact(emu, nprod):
 # its persistent grid (more 64 x 64 tiles than CUs, an even number of
 # k-blocks of 32, K <= 1024).  Depths 1 and 3 take the wide kernel when their
 # 256- or 128-row tiles number fewer than 256; depth 2 also for K > 1024;
-# depth 5 only for K > 1024.
+# depths 4 and 5 only for K > 1024.
 ROUTES = [
     (2100, 1900, 1500, 1, "32x32"),       # 270 tiles of 256 x 64, 47 k-blocks
     (1000, 1000, 1100, 1, "wide"),        # 64 tiles of 256 x 64, 35 k-blocks
@@ -184,7 +184,9 @@ ROUTES = [
     (2100, 1900, 1500, 6, "32x32"),       # 510 tiles of 128 x 64
     (1000, 900, 1100, 6, "wide"),         # 120 tiles of 128 x 64
     (1500, 1000, 640, 6, "persistent"),
-    (700, 600, 1100, 15, "wide"),         # long reduction, odd k-block count
+    (700, 600, 1100, 10, "wide"),         # long reduction, odd k-block count
+    (700, 600, 1000, 10, "32x32"),
+    (700, 600, 1100, 15, "wide"),
     (700, 600, 1000, 15, "32x32"),        # K <= 1024
 ]
 
