@@ -248,9 +248,11 @@ def main():
     achieved = p * flop / (g_avg * 1e-3) / 1e12
     kkey = f"{kind}:{p}:{n}"
     roofline = {
+        # d = 6 always runs the 16x16x32 kernel; d = 3 .. 5 pick one of the two
+        # DGEMM kernels by shape
         "kernel": ("gemm_f32_kernel" if kind == "sgemm" else
                    "gemm_f64w_kernel<d=6>" if p == 21 else
-                   f"gemm_f64_kernel<d={ {6: 3, 10: 4, 15: 5}[p]}>"),
+                   f"DGEMM GEMM launch, d={ {6: 3, 10: 4, 15: 5}[p]}"),
         "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
         "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
         "traffic": traffic_for(kkey),
