@@ -15,9 +15,9 @@
 // Two kernels.  gemm_f64_kernel (below): 32 x 32 x 16 MFMA, 4 waves in a 2 x 2
 // grid; wave tile (32 BM) x 32, output tile (64 BM) x 64.  gemm_f64w_kernel
 // (further down): 16 x 16 x 32 MFMA on a (16 BMW) x 32 wave tile, one barrier
-// per k-block; it runs depths d >= 6 (BMW = 1) and, with BMW = 2, the long
-// reductions of d = 2, 4, 5 and the small grids of d = 1 .. 3 (the choice is
-// made in launch_gemm_f64).  Per k-block of 32 the d planes of both operands are copied
+// per k-block; it runs depths d >= 6 (BMW = 1) and, with BMW = 2 or 4, the
+// long reductions of d = 1, 2, 4, 5 and the small grids of d = 1 .. 3 (the
+// choice is made in launch_gemm_f64).  Per k-block of 32 the d planes of both operands are copied
 // straight into LDS (global_load_lds_dwordx4) through a ring of LDS stages.
 // Each wave keeps one FP32 accumulator set per product for the whole panel
 // (all N_p live, so every fragment read from LDS feeds every product that
@@ -346,7 +346,8 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
 // and copies issued two trips ahead.  d = 6 runs here too: measured at
 // M = N = K = 8192 it is about 5 % faster than on the 32 x 32 kernel.
 // Depths d <= 5 (d planes per operand) can take a 32 x 32 wave tile here
-// (BMW = 2: 2 x 2 blocks, 16 registers per product, output tile 64 x 64).
+// (BMW = 2: 2 x 2 blocks, 16 registers per product, output tile 64 x 64) or,
+// with few products, 64 x 32 (BMW = 4, output tile 128 x 64).
 template <int D, int NS, bool ACC64_LDS, int BMW>
 struct CfgW {
     static constexpr int P = n_prod(D);
@@ -362,10 +363,10 @@ struct CfgW {
     static constexpr int MMAS = 2 * BMW * P;
     // AGPRs hold 32 / BMW products of 2 BMW blocks; later products use VGPRs
     static constexpr int Q_VGPR = P > 32 / BMW ? 32 / BMW : P;
-    static_assert(BMW == 1 || BMW == 2, "wave tile");
+    static_assert(BMW == 1 || BMW == 2 || BMW == 4, "wave tile");
     static_assert(4 * COPIES * 1024 == STAGE && 4 * A_COPIES * 1024 == NPL * A_BYTES,
                   "copy split");
-    static_assert(BMW == 2 || NPL == 6, "one-block tiles copy six planes");
+    static_assert(BMW != 1 || NPL == 6, "one-block tiles copy six planes");
     static_assert(NS * STAGE + ACC64_BYTES <= 160 * 1024, "LDS");
 };
 
@@ -374,7 +375,7 @@ struct CfgW {
 // 64 * is_B + 8 * plane + block.
 template <int D, int BMW>
 constexpr int read_code_w(int t) {
-    bool seen_a[6][2] = {}, seen_b[6][2] = {};
+    bool seen_a[6][4] = {}, seen_b[6][2] = {};
     int r = 0;
     for (int u = 0; u < 2 * BMW * n_prod(D); ++u) {
         const int q = u / (2 * BMW), a = (u % (2 * BMW)) / 2, b = u % 2, i = prod_i(q),
@@ -420,21 +421,24 @@ __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
     const int64_t b_plane = (int64_t)KB * RpadB * 64;
 
     // Copy c of a k-block by wave w moves 1 KB part g = 4 c + w of the list
-    // A parts (plane-major), then B parts: for BMW = 1, c < 3 moves part
-    // (w & 1) of A plane 2 c + (w >> 1); for BMW = 2, c < NPL moves part w of
-    // A plane c; the rest move part w of B plane c - A_COPIES.
+    // A parts (plane-major, 2 BMW parts a plane), then B parts: for BMW = 1,
+    // c < 3 moves part (w & 1) of A plane 2 c + (w >> 1); for BMW >= 2,
+    // c < A_COPIES moves part 4 (c % (BMW / 2)) + w of A plane c / (BMW / 2);
+    // the rest move part w of B plane c - A_COPIES.
     // ak, bk: the k-block's slab of plane 0 at the copied tile's first row.
     const int64_t a_off = BMW == 1 ? (int64_t)(wave >> 1) * a_plane + (wave & 1) * 1024
                                    : (int64_t)wave * 1024;
     const int a_dst = BMW == 1 ? (wave >> 1) * K::A_BYTES + (wave & 1) * 1024 : wave * 1024;
-    constexpr int A_STEP = BMW == 1 ? 2 : 1;             // A planes per copy index
     const int64_t b_off = (int64_t)wave * 1024;
     const int b_dst = K::NPL * K::A_BYTES + wave * 1024;
     auto issue_one = [&](const char *ak, const char *bk, char *base, auto c_c) {
         constexpr int c = decltype(c_c)::value;
+        // compile-time part of copy c's A offsets
+        constexpr int a_pl = BMW == 1 ? 2 * c : c / (BMW > 1 ? BMW / 2 : 1);
+        constexpr int a_pt = BMW == 1 ? 0 : 4 * (c % (BMW > 1 ? BMW / 2 : 1));
         if constexpr (c < K::A_COPIES)
-            copy_1k(ak + a_off + A_STEP * c * a_plane, base + a_dst + A_STEP * c * K::A_BYTES,
-                    lane16);
+            copy_1k(ak + a_off + a_pl * a_plane + a_pt * 1024,
+                    base + a_dst + a_pl * K::A_BYTES + a_pt * 1024, lane16);
         else
             copy_1k(bk + b_off + (c - K::A_COPIES) * b_plane,
                     base + b_dst + (c - K::A_COPIES) * K::B_BYTES, lane16);
@@ -687,9 +691,10 @@ hipError_t launch_gemm_f64(const uint16_t *Ap, const uint16_t *Bp, double *C, in
     // measured faster than the 32 x 32 x 16 kernel: long reductions (K > 1024)
     // of d = 2, 4 and 5 (8, 2 and 5 % at 8192^3), and grids of d = 1 .. 3
     // whose 128- or 256-row tiles would number fewer than the CUs (1.5 - 1.9x
-    // at 1000 x 1000 x 8200).  Short reductions of d = 2, 4, 5 and the large
-    // grids of d = 1 and 3 measured faster on the 32 x 32 x 16 kernel.  Both
-    // kernels give the same bits.
+    // at 1000 x 1000 x 8200).  The other long reductions of d = 1 take its
+    // 128 x 64 tiles (BMW = 4; 7-40 % faster).  Short reductions of d = 1, 2,
+    // 4, 5 and the large grids of d = 3 measured faster on the 32 x 32 x 16
+    // kernel.  Both kernels give the same bits.
     const int pw = persistent_workgroups();
     auto few_tiles = [&](int64_t mt) {
         return ((M + mt - 1) / mt) * ((N + DGEMM_NT - 1) / DGEMM_NT) < pw;
@@ -699,6 +704,8 @@ hipError_t launch_gemm_f64(const uint16_t *Ap, const uint16_t *Bp, double *C, in
         case 1:
             if (few_tiles(256))
                 return launch_w<1, 4, false, 2>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
+            if (long_k)
+                return launch_w<1, 4, false, 4, false>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
             return launch_t<1, 4, 4, false, 99>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
         case 2:
             if (long_k || few_tiles(128))

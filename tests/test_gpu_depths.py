@@ -171,13 +171,15 @@ def test_dgemm_persistent_large_tiles_bit_exact(emu, nprod):
 
 
 # (M, N, K, nprod, kernel the shape selects).  "32x32": the 32 x 32 x 16
-# kernel; "wide": the 16 x 16 x 32 kernel with 64 x 64 tiles; "persistent":
-# its persistent grid (more 64 x 64 tiles than CUs, an even number of
-# k-blocks of 32, K <= 1024).  Depths 1 and 3 take the wide kernel when their
-# 256- or 128-row tiles number fewer than 256; depth 2 also for K > 1024;
+# kernel; "wide": the 16 x 16 x 32 kernel with 64 x 64 tiles; "wide128": the
+# same with 128 x 64 tiles; "persistent": its persistent grid (more 64 x 64
+# tiles than CUs, an even number of k-blocks of 32, K <= 1024).  Depths 1 and
+# 3 take the wide kernel when their 256- or 128-row tiles number fewer than
+# 256; depths 1 and 2 also for K > 1024 (depth 1 then on 128 x 64 tiles);
 # depths 4 and 5 only for K > 1024.
 ROUTES = [
-    (2100, 1900, 1500, 1, "32x32"),       # 270 tiles of 256 x 64, 47 k-blocks
+    (2100, 1900, 1500, 1, "wide128"),     # 270 tiles of 256 x 64, 47 k-blocks
+    (2100, 1900, 640, 1, "32x32"),        # the same grid, short reduction
     (1000, 1000, 1100, 1, "wide"),        # 64 tiles of 256 x 64, 35 k-blocks
     (1500, 1000, 640, 3, "persistent"),   # 192 tiles of 128 x 64 -> 384 of 64 x 64
     (700, 600, 1100, 3, "wide"),          # long reduction
