@@ -1,0 +1,92 @@
+"""DGEMM parity at the shape boundaries where the library changes kernel or
+grid, and at seeded random shapes over every product count.
+
+The library picks, by shape, between the 32 x 32 x 16 kernel and the
+16 x 16 x 32 kernel (64 x 64 or 128 x 64 tiles), and between one workgroup per
+tile and a persistent grid (K <= 1024, more tiles than CUs, and for the
+16 x 16 x 32 kernel an even number of k-blocks).  None of these choices may
+change a bit of the result (Eq. fp64reconstruction with the executed order of
+Sec. 6.3): sampled entries, corners included, are compared bit for bit with the
+oracle.  Inputs are seeded and synthetic."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import seeded_inputs as S
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def emu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_04663_amd as E
+    E.lib()
+    return E
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def check_sampled(emu, M, N, K, nprod, seed, nsample=160):
+    A = S.make("wide", seed, (M, K), np.float64)
+    B = S.make("uniform", seed + 1, (K, N), np.float64)
+    C = emu.dgemm(dev(A), dev(B), nprod).cpu().numpy()
+    rng = np.random.default_rng(seed)
+    r = np.concatenate([[0, M - 1, 0, M - 1], rng.integers(0, M, nsample)]).astype(np.int64)
+    c = np.concatenate([[0, 0, N - 1, N - 1], rng.integers(0, N, nsample)]).astype(np.int64)
+    ref, st = O.emu_dgemm_entries(A, B, r, c, nprod)
+    assert st == 0
+    got = np.ascontiguousarray(C[r, c])
+    assert np.array_equal(got.view(np.uint64), ref.view(np.uint64)), (M, N, K, nprod)
+
+
+# (M, N, K, nprod): both sides of each boundary
+BOUNDARIES = [
+    # K = 1024 is the last short reduction (32 k-blocks), 1025 the first long one
+    (1100, 1100, 1024, 3), (1100, 1100, 1025, 3),
+    (1100, 1100, 1024, 10), (1100, 1100, 1025, 10),
+    (1100, 1100, 1024, 15), (1100, 1100, 1025, 15),
+    (1100, 1100, 1024, 1), (1100, 1100, 1025, 1),
+    # 256 tiles of 128 x 64 (d = 2, 3) or 256 x 64 (d = 1) is not "few"; 248 is
+    (1024, 1984, 640, 6), (1024, 2048, 640, 6),
+    (1024, 1984, 640, 3), (1024, 2048, 640, 3),
+    (2048, 1984, 1100, 1), (2048, 2048, 1100, 1),
+    # d = 6: exactly 256 tiles of 32 x 64 take one workgroup per tile, 272 a
+    # persistent grid
+    (512, 1024, 640, 21), (544, 1024, 640, 21),
+    # odd k-block count with more tiles than CUs (the 16x16x32 kernel then
+    # takes one tile per workgroup)
+    (1040, 1100, 608, 21), (1040, 1100, 608, 36),
+]
+
+
+@pytest.mark.parametrize("M,N,K,nprod", BOUNDARIES)
+def test_kernel_choice_boundaries_bit_exact(emu, M, N, K, nprod):
+    check_sampled(emu, M, N, K, nprod, seed=7000 + M + N + K + nprod)
+
+
+def _random_cases(n=20, seed=20260):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        M = int(rng.integers(1, 1400))
+        N = int(rng.integers(1, 1400))
+        K = int(rng.integers(1, 2300))
+        nprod = int(rng.choice([1, 3, 6, 10, 15, 21, 26, 30, 33, 35, 36]))
+        out.append((M, N, K, nprod))
+    return out
+
+
+@pytest.mark.parametrize("M,N,K,nprod", _random_cases())
+def test_random_shapes_bit_exact(emu, M, N, K, nprod):
+    check_sampled(emu, M, N, K, nprod, seed=9000 + M * 7 + N * 3 + K + nprod, nsample=96)
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 1, 1), (1, 700, 1300), (700, 1, 1300), (65, 3, 2049)])
+@pytest.mark.parametrize("nprod", [1, 10, 21])
+def test_degenerate_extents_bit_exact(emu, M, N, K, nprod):
+    check_sampled(emu, M, N, K, nprod, seed=11000 + M + N + K + nprod, nsample=32)
