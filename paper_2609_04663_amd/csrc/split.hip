@@ -256,8 +256,18 @@ __device__ __forceinline__ void split_f64_pass(const F64SplitOperand op, int64_t
                                F64SplitState *out, unsigned *status) {
     __shared__ unsigned long long red[6][SPLIT_THREADS / 64];
     double sig[6];
+    // Levels whose slices are normal BF16 values whenever the chain is right:
+    // every Z is a multiple of 2^(v - 8) of magnitude <= 2^v, so for
+    // -118 <= v <= 127 a nonzero Z lies in [2^-126, 2^127] and needs at most 8
+    // significant bits.  There the BF16 pattern is the top half of (float) Z,
+    // the residual is A - Z, and only a non-finite Z (NaN or Inf input) can
+    // raise a flag.  Other levels take the general rounding and checks.
+    bool plain[6];
 #pragma unroll
-    for (int r = 0; r < 6; ++r) sig[r] = (v[r] == V_ZERO) ? 0.0 : ldexp(cst, v[r] + 45);
+    for (int r = 0; r < 6; ++r) {
+        sig[r] = (v[r] == V_ZERO) ? 0.0 : ldexp(cst, v[r] + 45);
+        plain[r] = v[r] != V_ZERO && v[r] >= -118 && v[r] <= 127;
+    }
     double mx[6] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
     unsigned st = 0;
     const int RG = (int)(op.Rpad / ROWS_PER_BLOCK);
@@ -299,7 +309,13 @@ __device__ __forceinline__ void split_f64_pass(const F64SplitOperand op, int64_t
             for (int r = 0; r < 6; ++r) {
                 if (r >= nlev) break;
                 u16 h = 0;
-                if (v[r] != V_ZERO) {
+                if (plain[r]) {
+                    const double t = w + sig[r];
+                    const double z = t - sig[r];
+                    h = (u16)(__float_as_uint((float)z) >> 16);
+                    if ((h & 0x7F80u) == 0x7F80u) st |= ST_OVERFLOW;
+                    w = w - z;
+                } else if (v[r] != V_ZERO) {
                     const double t = w + sig[r];
                     const double z = t - sig[r];
                     h = bf16_rne_bits((float)z);          // exact for in-domain slices
