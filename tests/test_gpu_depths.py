@@ -137,9 +137,10 @@ def test_dgemm_rowcol_depths_bit_exact(emu, nprod):
 def test_dgemm_persistent_tiles_bit_exact(emu, K, nprod):
     """More output tiles than CUs and a short reduction: both DGEMM kernels run
     persistent workgroups that walk several tiles each, the copy ring running
-    on across tile boundaries.  The d >= 6 kernel needs an even k-block count
-    (K = 640) and takes one tile per workgroup otherwise (K = 600); the d <= 5
-    kernel (nprod 10, 15: 324 tiles of 64 x 64) takes either.  Sampled entries,
+    on across tile boundaries.  The 16 x 16 x 32 kernel (nprod 21, 36) needs an
+    even k-block count (K = 640) and takes one tile per workgroup otherwise
+    (K = 600); the 32 x 32 x 16 kernel (nprod 10, 15 at these short
+    reductions: 324 tiles of 64 x 64) takes either.  Sampled entries,
     including the last tile row and column."""
     M = N = 1100
     A = S.make("wide", 961, (M, K), np.float64)
