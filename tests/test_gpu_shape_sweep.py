@@ -90,3 +90,42 @@ def test_random_shapes_bit_exact(emu, M, N, K, nprod):
 @pytest.mark.parametrize("nprod", [1, 10, 21])
 def test_degenerate_extents_bit_exact(emu, M, N, K, nprod):
     check_sampled(emu, M, N, K, nprod, seed=11000 + M + N + K + nprod, nsample=32)
+
+
+def _random_forms(n=40, seed=31337):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        big = rng.random() < 0.3
+        M = int(rng.integers(1, 2600 if big else 700))
+        N = int(rng.integers(1, 2600 if big else 700))
+        K = int(rng.integers(1, 2600))
+        nprod = int(rng.choice([1, 3, 6, 10, 15, 21, 26, 30, 33, 35, 36]))
+        out.append((M, N, K, nprod, str(rng.choice(["N", "T"])), str(rng.choice(["N", "T"])),
+                    bool(rng.random() < 0.25)))
+    return out
+
+
+@pytest.mark.parametrize("M,N,K,nprod,ta,tb,rowcol", _random_forms())
+def test_random_forms_and_scopes_bit_exact(emu, M, N, K, nprod, ta, tb, rowcol):
+    """Seeded random shapes with transposed operands (op(A), op(B) of the BLAS
+    form) and, for a quarter of them, the row/column exponent scope."""
+    seed = 13000 + M + 3 * N + 7 * K + nprod
+    A = S.make("wide", seed, (M, K), np.float64)
+    B = S.make("normal", seed + 1, (K, N), np.float64)
+    sA = np.ascontiguousarray(A.T) if ta == "T" else A
+    sB = np.ascontiguousarray(B.T) if tb == "T" else B
+    if rowcol:
+        emu.set_split_scope(emu.SCOPE_ROWCOL)
+    try:
+        C = emu.dgemm_ex(dev(sA), dev(sB), nprod, None, ta, tb).cpu().numpy()
+    finally:
+        emu.set_split_scope(emu.SCOPE_OPERAND)
+    rng = np.random.default_rng(seed)
+    r = np.concatenate([[0, M - 1], rng.integers(0, M, 62)]).astype(np.int64)
+    c = np.concatenate([[N - 1, 0], rng.integers(0, N, 62)]).astype(np.int64)
+    ref, st = O.emu_dgemm_entries(A, B, r, c, nprod,
+                                  scope=O.SCOPE_ROWCOL if rowcol else O.SCOPE_OPERAND)
+    assert st == 0
+    got = np.ascontiguousarray(C[r, c])
+    assert np.array_equal(got.view(np.uint64), ref.view(np.uint64))
