@@ -129,3 +129,43 @@ def test_random_forms_and_scopes_bit_exact(emu, M, N, K, nprod, ta, tb, rowcol):
     assert st == 0
     got = np.ascontiguousarray(C[r, c])
     assert np.array_equal(got.view(np.uint64), ref.view(np.uint64))
+
+
+def _random_sgemm_forms(n=30, seed=4242):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        big = rng.random() < 0.3
+        M = int(rng.integers(1, 2600 if big else 700))
+        N = int(rng.integers(1, 2600 if big else 700))
+        K = int(rng.integers(1, 3000))
+        out.append((M, N, K, str(rng.choice(["N", "T"])), str(rng.choice(["N", "T"]))))
+    return out
+
+
+@pytest.mark.parametrize("M,N,K,ta,tb", _random_sgemm_forms())
+def test_sgemm_random_forms_within_bounds(emu, M, N, K, ta, tb):
+    """Emulated SGEMM at seeded random shapes (single pass and split-K, both
+    operand orientations): every sampled entry within the per-entry bound of
+    the omitted products plus the chunked FP32 accumulation, and the sample's
+    normwise error within 4 K 2^-24, against a double-double reference."""
+    import math
+    seed = 17000 + M + 3 * N + 7 * K
+    A = S.make("normal", seed, (M, K), np.float32)
+    B = S.make("normal", seed + 1, (K, N), np.float32)
+    sA = np.ascontiguousarray(A.T) if ta == "T" else A
+    sB = np.ascontiguousarray(B.T) if tb == "T" else B
+    C = emu.sgemm_ex(dev(sA), dev(sB), None, ta, tb).cpu().numpy()
+    rng = np.random.default_rng(seed)
+    r = np.concatenate([[0, M - 1], rng.integers(0, M, 94)]).astype(np.int64)
+    c = np.concatenate([[N - 1, 0], rng.integers(0, N, 94)]).astype(np.int64)
+    hi, lo = O.ref_dd_entries(A, B, r, c)
+    ab = O.absprod_entries(A, B, r, c)
+    got = np.ascontiguousarray(C[r, c]).astype(np.float64)
+    err = np.abs((got - hi) - lo)
+    esc_cap = 2.0 ** -22 + (6 * 256 + math.ceil(K / 256)) * 2.0 ** -24
+    nz = ab > 0
+    assert np.all(err[~nz] == 0.0)
+    assert np.all(err[nz] <= esc_cap * ab[nz])
+    if np.any(hi):
+        assert np.sqrt(np.sum(err ** 2)) <= 4 * K * 2.0 ** -24 * np.sqrt(np.sum(hi ** 2))
