@@ -299,9 +299,10 @@ int emu_sgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, floa
         hipError_t e = launch_scale_c_f32(C, M, N, ldc, beta, g_stream);
         return e == hipSuccess ? EMU_OK : hip_fail(e, "scale C");
     }
-    const Shape s = plan(M, N, K, 3, SGEMM_MT, SGEMM_NT);
+    const int tile_m = sgemm_tile_m(M, N, (K + KBLK - 1) / KBLK);
+    const Shape s = plan(M, N, K, 3, tile_m, SGEMM_NT);
     // few output tiles: split the reduction (partial sums after the planes)
-    const int splits = sgemm_splits(M, N, s.KB);
+    const int splits = sgemm_splits(M, N, s.KB, tile_m);
     const size_t part_off = (s.bytesA + s.bytesB + 255) / 256 * 256;
     const size_t part_bytes = splits > 1 ? (size_t)splits * M * N * sizeof(float) : 0;
     rc = ensure_workspace(part_off + part_bytes);
@@ -317,8 +318,8 @@ int emu_sgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, floa
     hipError_t e = launch_split_f32(ops, 2, s.KB, ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f32");
     prof_mark(1);
-    e = launch_gemm_f32(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, alpha, beta, splits, part,
-                        g_stream);
+    e = launch_gemm_f32(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, alpha, beta, tile_m, splits,
+                        part, g_stream);
     if (e != hipSuccess) return hip_fail(e, "gemm_f32");
     prof_mark(2);
     return EMU_OK;

@@ -31,7 +31,7 @@ constexpr int ROW_GROUP = 64;   // packed rows are padded to a multiple of this 
 constexpr int KPANEL = 256;     // reduction panel B_K of the FP32/FP64 reconstruction
 
 // ... and of the GEMM tile that reads them (output tile rows for A, columns for B).
-constexpr int SGEMM_MT = 192, SGEMM_NT = 128;
+constexpr int SGEMM_NT = 128;   // SGEMM output tiles: (192 or 128) x 128
 constexpr int DGEMM_NT = 64;
 inline int dgemm_mt(int d) { return d == 1 ? 256 : d <= 3 ? 128 : 64; }
 // Slices of each operand that the products of depth d read (indices < 6).
@@ -117,10 +117,11 @@ hipError_t launch_copy_v(const F64SplitState *st, int32_t *v, hipStream_t s);
 // Split-K factor of the emulated SGEMM: 1 unless the output tiles fill at most
 // half of the chip, else up to 16 splits of whole reduction panels.  splits > 1 needs part:
 // splits x M x N floats of scratch for the partial sums.
-int sgemm_splits(int64_t M, int64_t N, int64_t KB);
+int sgemm_tile_m(int64_t M, int64_t N, int64_t KB);   // 192 or 128 output rows per tile
+int sgemm_splits(int64_t M, int64_t N, int64_t KB, int tile_m);
 hipError_t launch_gemm_f32(const uint16_t *Ap, const uint16_t *Bp, float *C, int64_t M, int64_t N,
                            int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc, float alpha,
-                           float beta, int splits, float *part, hipStream_t s);
+                           float beta, int tile_m, int splits, float *part, hipStream_t s);
 // sa, sb: row weights of A and column weights of B to restore (C_mn times
 // 2^(sa_m + sb_n)), or both null
 hipError_t launch_gemm_f64(const uint16_t *Ap, const uint16_t *Bp, double *C, int64_t M,

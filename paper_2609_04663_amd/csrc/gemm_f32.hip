@@ -2,9 +2,10 @@
 // Sec. 4.2, on bf16 MFMA (v_mfma_f32_32x32x16_bf16) with FP32 accumulation.
 //
 // Workgroup: 256 threads = 4 waves in a 2 x 2 grid, output tile 192 x 128,
-// wave tile 96 x 64 (3 x 2 MFMA blocks of 32 x 32).  Per k-block of 32
-// reduction indices the three BF16 planes of both operands (3 x 12 KB of A,
-// 3 x 8 KB of B) are copied straight from the packed buffers into LDS with
+// wave tile 96 x 64 (3 x 2 MFMA blocks of 32 x 32); a 128 x 128 tile (wave
+// 64 x 64) serves grids whose 192-row tiles would leave CUs idle.  Per k-block
+// of 32 reduction indices the three BF16 planes of both operands (3 x 12 KB of
+// A, 3 x 8 KB of B) are copied straight from the packed buffers into LDS with
 // global_load_lds_dwordx4, double-buffered, so the copy of k-block kb + 1
 // overlaps the MFMAs of k-block kb.  Each wave reads every fragment once per
 // 16-index sub-step and issues all six products on it: B fragments of the three
@@ -26,17 +27,18 @@
 namespace emu {
 namespace {
 
-constexpr int MT = SGEMM_MT, NT = SGEMM_NT, NC = 3, RB = MT / 64;
-constexpr int A_BYTES = MT * 64;                    // one plane, one k-block
-constexpr int B_BYTES = NT * 64;
-constexpr int STAGE = NC * (A_BYTES + B_BYTES);     // 60 KB
-constexpr int A_CHUNKS = NC * A_BYTES / 1024;       // 36
-constexpr int B_CHUNKS = NC * B_BYTES / 1024;       // 24
+constexpr int NT = SGEMM_NT, NC = 3;
 
+// RB 32-row blocks per wave: output tile (64 RB) x 128, wave tile (32 RB) x 64.
+template <int RB>
 __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
     const uint16_t *__restrict__ Ap, const uint16_t *__restrict__ Bp, float *__restrict__ C,
     int64_t M, int64_t N, int KB, int64_t RpadA, int64_t RpadB, int64_t ldc, float alpha,
     float beta, int nt_m, int nt_n, int kb_per_split, float *__restrict__ part) {
+    constexpr int MT = 64 * RB;
+    constexpr int A_BYTES = MT * 64;                    // one plane, one k-block
+    constexpr int B_BYTES = NT * 64;
+    constexpr int STAGE = NC * (A_BYTES + B_BYTES);     // 60 KB (RB = 3), 48 KB (RB = 2)
     __shared__ __attribute__((aligned(1024))) char stage0[STAGE];
     __shared__ __attribute__((aligned(1024))) char stage1[STAGE];
 
@@ -53,24 +55,24 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
     const int64_t a_plane = (int64_t)KB * RpadA * 64;
     const int64_t b_plane = (int64_t)KB * RpadB * 64;
 
-    // Copy issue for one k-block: wave w moves 1 KB parts [3w, 3w + 3) of each A
-    // plane and [2w, 2w + 2) of each B plane, so every address is a wave-uniform
-    // base plus a compile-time offset.  Copy j < 9 is A plane j / 3, part j % 3;
-    // copy 9 + j is B plane j / 2, part j % 2.
-    static_assert(A_BYTES / 1024 == 12 && B_BYTES / 1024 == 8, "part split assumes 192 x 128");
-    constexpr int COPIES = 15;
-    const int64_t a_base = m0 * 64 + wave * 3 * 1024;
+    // Copy issue for one k-block: wave w moves 1 KB parts [RB w, RB w + RB) of
+    // each A plane and [2w, 2w + 2) of each B plane, so every address is a
+    // wave-uniform base plus a compile-time offset.  Copy j < 3 RB is A plane
+    // j / RB, part j % RB; copy 3 RB + j is B plane j / 2, part j % 2.
+    static_assert(A_BYTES / 1024 == 4 * RB && B_BYTES / 1024 == 8, "part split");
+    constexpr int AC = NC * RB, COPIES = AC + 6;
+    const int64_t a_base = m0 * 64 + wave * RB * 1024;
     const int64_t b_base = n0 * 64 + wave * 2 * 1024;
     auto issue_one = [&](int kb, char *base, auto j_c) {
         constexpr int j = decltype(j_c)::value;
-        if constexpr (j < 9)
-            copy_1k(Ag + (int64_t)kb * RpadA * 64 + a_base + (j / 3) * a_plane + (j % 3) * 1024,
-                    base + wave * 3 * 1024 + (j / 3) * A_BYTES + (j % 3) * 1024, lane16);
+        if constexpr (j < AC)
+            copy_1k(Ag + (int64_t)kb * RpadA * 64 + a_base + (j / RB) * a_plane + (j % RB) * 1024,
+                    base + wave * RB * 1024 + (j / RB) * A_BYTES + (j % RB) * 1024, lane16);
         else
-            copy_1k(Bg + (int64_t)kb * RpadB * 64 + b_base + ((j - 9) / 2) * b_plane +
-                        ((j - 9) % 2) * 1024,
-                    base + NC * A_BYTES + wave * 2 * 1024 + ((j - 9) / 2) * B_BYTES +
-                        ((j - 9) % 2) * 1024,
+            copy_1k(Bg + (int64_t)kb * RpadB * 64 + b_base + ((j - AC) / 2) * b_plane +
+                        ((j - AC) % 2) * 1024,
+                    base + NC * A_BYTES + wave * 2 * 1024 + ((j - AC) / 2) * B_BYTES +
+                        ((j - AC) % 2) * 1024,
                     lane16);
     };
 
@@ -92,13 +94,13 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
     auto read_b = [&](const char *base, int off, int c, int cb) {
         return lds_frag(base + bt0 + c * B_BYTES + cb * 32 * 64, off);
     };
-    // One sub-step in 36 slots.  MFMA t is product g = t / 6 of
-    // (A0B0 | A0B1 A0B2 A1B0 A1B1 A2B0) on block (rb, cb) = ((t % 6) / 2, t % 2):
+    // One sub-step in 12 RB slots.  MFMA t is product g = t / G (G = 2 RB) of
+    // (A0B0 | A0B1 A0B2 A1B0 A1B1 A2B0) on block (rb, cb) = ((t % G) / 2, t % 2):
     // A0B0 goes to hi, the five smaller products to lo, product-major so that
     // consecutive MFMAs never share an accumulator.  After MFMA t come the reads
     // of the next sub-step (stage nbase, lane offset noff) of the fragments whose
     // last use was MFMA t, then copy t / 2 of k-block ckb (even t, t / 2 < NCOPY).
-    // Latency cover of every read: at least 12 MFMAs.
+    // Latency cover of every read: at least 4 RB MFMAs.
     // zero: the panel's first sub-step (hi starts at 0); zero_lo: the first
     // sub-step of the whole reduction (lo starts at 0).
     constexpr int PI[6] = {0, 0, 0, 1, 1, 2}, PJ[6] = {0, 1, 2, 0, 1, 0};
@@ -108,10 +110,10 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
         constexpr bool zero = decltype(zero_c)::value;
         constexpr bool zero_lo = decltype(zero_lo_c)::value;
         constexpr int NCOPY = decltype(ncopy_c)::value;
-        static_assert(RB == 3, "last-use slots below assume three row blocks");
-        static_for<36>([&](auto t_c) {
+        constexpr int G = 2 * RB;
+        static_for<12 * RB>([&](auto t_c) {
             constexpr int t = decltype(t_c)::value;
-            constexpr int g = t / 6, rb = (t % 6) / 2, cb = t % 2;
+            constexpr int g = t / G, rb = (t % G) / 2, cb = t % 2;
             constexpr int i = PI[g], j = PJ[g];
             const bf16x8 &bop = (j == 0) ? b0[cb] : f.b[j][cb];
             if constexpr (g == 0)
@@ -119,14 +121,17 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
             else
                 lo[rb][cb] = mfma(f.a[i][rb], bop, (zero_lo && g == 1) ? f32x16{} : lo[rb][cb]);
             order_fence();
-            // last uses: B0 -> second buffer at t = 0, 1; A0[r] at 13 + 2r; B2[c] at
-            // 16 + c; A1[r] at 25 + 2r; B1[c] at 28 + c; A2[r] at 31 + 2r
+            // last uses: B0 -> second buffer at t = 0, 1; A0[r] at 2G + 1 + 2r;
+            // B2[c] at 3G - 2 + c; A1[r] at 4G + 1 + 2r; B1[c] at 5G - 2 + c;
+            // A2[r] at 5G + 1 + 2r (RB = 3: 13 + 2r, 16 + c, 25 + 2r, 28 + c, 31 + 2r)
+            constexpr int ua0 = t - (2 * G + 1), ua1 = t - (4 * G + 1), ua2 = t - (5 * G + 1);
+            constexpr int ub2 = t - (3 * G - 2), ub1 = t - (5 * G - 2);
             if constexpr (t < 2) b0n[t] = read_b(nbase, noff, 0, t);
-            if constexpr (t == 13 || t == 15 || t == 17) f.a[0][(t - 13) / 2] = read_a(nbase, noff, 0, (t - 13) / 2);
-            if constexpr (t == 16 || t == 17) f.b[2][t - 16] = read_b(nbase, noff, 2, t - 16);
-            if constexpr (t == 25 || t == 27 || t == 29) f.a[1][(t - 25) / 2] = read_a(nbase, noff, 1, (t - 25) / 2);
-            if constexpr (t == 28 || t == 29) f.b[1][t - 28] = read_b(nbase, noff, 1, t - 28);
-            if constexpr (t == 31 || t == 33 || t == 35) f.a[2][(t - 31) / 2] = read_a(nbase, noff, 2, (t - 31) / 2);
+            if constexpr (ua0 >= 0 && ua0 % 2 == 0 && ua0 / 2 < RB) f.a[0][ua0 / 2] = read_a(nbase, noff, 0, ua0 / 2);
+            if constexpr (ub2 == 0 || ub2 == 1) f.b[2][ub2] = read_b(nbase, noff, 2, ub2);
+            if constexpr (ua1 >= 0 && ua1 % 2 == 0 && ua1 / 2 < RB) f.a[1][ua1 / 2] = read_a(nbase, noff, 1, ua1 / 2);
+            if constexpr (ub1 == 0 || ub1 == 1) f.b[1][ub1] = read_b(nbase, noff, 1, ub1);
+            if constexpr (ua2 >= 0 && ua2 % 2 == 0 && ua2 / 2 < RB) f.a[2][ua2 / 2] = read_a(nbase, noff, 2, ua2 / 2);
             order_fence();
             if constexpr (t % 2 == 0 && t / 2 < NCOPY)
                 issue_one(ckb, cdst, std::integral_constant<int, t / 2>{});
@@ -235,30 +240,75 @@ __global__ void reduce_splits_kernel(const float *__restrict__ part, int splits,
 
 }  // namespace
 
-int sgemm_splits(int64_t M, int64_t N, int64_t KB) {
-    const int64_t tiles = ((M + MT - 1) / MT) * ((N + NT - 1) / NT);
+// CUs of the current device (256 on MI355X), read once.
+static int device_cus() {
+    static int cus = 0;
+    if (cus == 0) {
+        int dev = 0, n = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            n < 1)
+            n = 256;
+        cus = n;
+    }
+    return cus;
+}
+
+int sgemm_splits(int64_t M, int64_t N, int64_t KB, int tile_m) {
+    const int64_t cus = device_cus();
+    const int64_t tiles = ((M + tile_m - 1) / tile_m) * ((N + NT - 1) / NT);
     const int64_t panels = (KB + KB_PER_PANEL - 1) / KB_PER_PANEL;
-    // split only when the tiles fill at most half of the 256 CUs, and keep all
+    // split only when the tiles fill at most half of the CUs, and keep all
     // splits within one wave of workgroups (the partial sums cost a pass)
-    if (2 * tiles > 256 || panels < 2) return 1;
-    int64_t sp = 256 / tiles;
+    if (2 * tiles > cus || panels < 2) return 1;
+    int64_t sp = cus / tiles;
     sp = sp < panels ? sp : panels;
     sp = sp < 16 ? sp : 16;
     const int64_t per = (panels + sp - 1) / sp;             // whole panels per split
     return (int)((panels + per - 1) / per);
 }
 
+int sgemm_tile_m(int64_t M, int64_t N, int64_t KB) {
+    // One workgroup per CU runs at a time (120 or 96 KB of LDS).  Model the
+    // time of each tile height as rounds of workgroups x rows per tile x
+    // k-blocks per split, the 128-row tile's larger copy share per MFMA counted
+    // as 5 %, and take the shorter (measured: 128 rows are 18-28 % faster at
+    // 2048^3 and 2560^3, 4-13 % at 1024^3, 4096^3 and 1024 x 1024 x 65536;
+    // 192 rows 2-19 % faster at 3072^3, 6144^3, 16384 x 16384 x 512 and
+    // 3000 x 2000 x 4000).
+    const int64_t cus = device_cus();
+    double best = 0.0;
+    int pick = 192;
+    for (int t : {192, 128}) {
+        const int64_t tiles = ((M + t - 1) / t) * ((N + NT - 1) / NT);
+        const int64_t sp = sgemm_splits(M, N, KB, t);
+        const int64_t rounds = (tiles * sp + cus - 1) / cus;
+        const double cost = (double)rounds * t * (double)((KB + sp - 1) / sp) * (t == 128 ? 1.05 : 1.0);
+        if (t == 192 || cost < best) {
+            best = cost;
+            pick = t;
+        }
+    }
+    return pick;
+}
+
 hipError_t launch_gemm_f32(const uint16_t *Ap, const uint16_t *Bp, float *C, int64_t M, int64_t N,
                            int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc, float alpha,
-                           float beta, int splits, float *part, hipStream_t s) {
-    const int nt_m = (int)((M + MT - 1) / MT), nt_n = (int)((N + NT - 1) / NT);
+                           float beta, int tile_m, int splits, float *part, hipStream_t s) {
+    if (tile_m != 192 && tile_m != 128) return hipErrorInvalidValue;
+    const int nt_m = (int)((M + tile_m - 1) / tile_m), nt_n = (int)((N + NT - 1) / NT);
     const int64_t panels = (KB + KB_PER_PANEL - 1) / KB_PER_PANEL;
     const int kb_per_split = (int)((panels + splits - 1) / splits) * KB_PER_PANEL;
     if (splits < 1 || (splits > 1 && !part) || (int64_t)(splits - 1) * kb_per_split >= KB)
         return hipErrorInvalidValue;
-    gemm_f32_kernel<<<dim3(nt_m * nt_n, splits), 256, 0, s>>>(
-        Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc, alpha, beta, nt_m, nt_n, kb_per_split,
-        splits > 1 ? part : nullptr);
+    const dim3 grid(nt_m * nt_n, splits);
+    float *pp = splits > 1 ? part : nullptr;
+    if (tile_m == 192)
+        gemm_f32_kernel<3><<<grid, 256, 0, s>>>(Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc, alpha,
+                                                beta, nt_m, nt_n, kb_per_split, pp);
+    else
+        gemm_f32_kernel<2><<<grid, 256, 0, s>>>(Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc, alpha,
+                                                beta, nt_m, nt_n, kb_per_split, pp);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || splits == 1) return e;
     const int64_t total = M * N;

@@ -169,3 +169,35 @@ def test_sgemm_random_forms_within_bounds(emu, M, N, K, ta, tb):
     assert np.all(err[nz] <= esc_cap * ab[nz])
     if np.any(hi):
         assert np.sqrt(np.sum(err ** 2)) <= 4 * K * 2.0 ** -24 * np.sqrt(np.sum(hi ** 2))
+
+
+# (M, N, K, tile rows, splits) the SGEMM picks: both tile heights, with and
+# without split-K, ragged in every dimension
+SGEMM_ROUTES = [
+    (3001, 1999, 1111, 192, 1),
+    (2990, 2100, 777, 128, 1),
+    (1530, 1540, 1600, 192, 2),
+    (1000, 900, 5000, 128, 4),
+    (700, 600, 3000, 192, 12),
+    (2048, 2048, 2048, 128, 1),
+]
+
+
+@pytest.mark.parametrize("M,N,K,tile,splits", SGEMM_ROUTES)
+def test_sgemm_tile_routes_within_bounds(emu, M, N, K, tile, splits):
+    """Each SGEMM configuration the shape can select (192- or 128-row tiles,
+    one pass or split-K), checked like the random cases above."""
+    import math
+    seed = 19000 + M + N + K
+    A = S.make("uniform", seed, (M, K), np.float32)
+    B = S.make("normal", seed + 1, (K, N), np.float32)
+    C = emu.sgemm(dev(A), dev(B)).cpu().numpy()
+    rng = np.random.default_rng(seed)
+    r = np.concatenate([[0, M - 1, M - 1, 0], rng.integers(0, M, 124)]).astype(np.int64)
+    c = np.concatenate([[0, N - 1, 0, N - 1], rng.integers(0, N, 124)]).astype(np.int64)
+    hi, lo = O.ref_dd_entries(A, B, r, c)
+    ab = O.absprod_entries(A, B, r, c)
+    err = np.abs((np.ascontiguousarray(C[r, c]).astype(np.float64) - hi) - lo)
+    esc_cap = 2.0 ** -22 + (6 * 256 + math.ceil(K / 256)) * 2.0 ** -24
+    assert np.all(err <= esc_cap * ab)
+    assert np.sqrt(np.sum(err ** 2)) <= 4 * K * 2.0 ** -24 * np.sqrt(np.sum(hi ** 2))
