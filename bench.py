@@ -107,8 +107,8 @@ def main():
         print(json.dumps({k: source_hash(v) for k, v in KERNEL_SOURCES.items()}))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(how the computation would shard is described in DESIGN.md).", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(--gpus must be 1).", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -1,6 +1,7 @@
 """GPU parity: the HIP path (through the C ABI) against the CPU oracle.
 
-Bars (the design doc derives them):
+Bars (from the exactness of the panel products, Sec. 4.3, and the omitted
+products plus FP32 accumulation of the SGEMM, Sec. 4.2):
   * component planes, slices and exponents: bit-exact;
   * emulated DGEMM: bit-exact (every panel product is an exact FP32 value, so
     both sides add the same FP64 numbers in the same order);
