@@ -12,6 +12,23 @@
 #include "../../include/emu.h"
 #include "emu_internal.h"
 
+namespace emu {
+
+int device_cu_count() {
+    static int cus = 0;
+    if (cus == 0) {
+        int dev = 0, n = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            n < 1)
+            n = 256;
+        cus = n;
+    }
+    return cus;
+}
+
+}  // namespace emu
+
 namespace {
 
 using namespace emu;

@@ -117,6 +117,8 @@ hipError_t launch_copy_v(const F64SplitState *st, int32_t *v, hipStream_t s);
 // Split-K factor of the emulated SGEMM: 1 unless the output tiles fill at most
 // half of the chip, else up to 16 splits of whole reduction panels.  splits > 1 needs part:
 // splits x M x N floats of scratch for the partial sums.
+// CUs of the current device (256 on MI355X), read once per process.
+int device_cu_count();
 int sgemm_tile_m(int64_t M, int64_t N, int64_t KB);   // 192 or 128 output rows per tile
 int sgemm_splits(int64_t M, int64_t N, int64_t KB, int tile_m);
 hipError_t launch_gemm_f32(const uint16_t *Ap, const uint16_t *Bp, float *C, int64_t M, int64_t N,

@@ -240,22 +240,8 @@ __global__ void reduce_splits_kernel(const float *__restrict__ part, int splits,
 
 }  // namespace
 
-// CUs of the current device (256 on MI355X), read once.
-static int device_cus() {
-    static int cus = 0;
-    if (cus == 0) {
-        int dev = 0, n = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            n < 1)
-            n = 256;
-        cus = n;
-    }
-    return cus;
-}
-
 int sgemm_splits(int64_t M, int64_t N, int64_t KB, int tile_m) {
-    const int64_t cus = device_cus();
+    const int64_t cus = device_cu_count();
     const int64_t tiles = ((M + tile_m - 1) / tile_m) * ((N + NT - 1) / NT);
     const int64_t panels = (KB + KB_PER_PANEL - 1) / KB_PER_PANEL;
     // split only when the tiles fill at most half of the CUs, and keep all
@@ -276,7 +262,7 @@ int sgemm_tile_m(int64_t M, int64_t N, int64_t KB) {
     // 2048^3 and 2560^3, 4-13 % at 1024^3, 4096^3 and 1024 x 1024 x 65536;
     // 192 rows 2-19 % faster at 3072^3, 6144^3, 16384 x 16384 x 512 and
     // 3000 x 2000 x 4000).
-    const int64_t cus = device_cus();
+    const int64_t cus = device_cu_count();
     double best = 0.0;
     int pick = 192;
     for (int t : {192, 128}) {

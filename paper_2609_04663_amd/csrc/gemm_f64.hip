@@ -617,16 +617,8 @@ __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
 // Persistent grid of the DGEMM kernels: one workgroup per CU (their LDS use
 // allows one), rounded down to a multiple of 8.
 int persistent_workgroups() {
-    static int g = 0;
-    if (g == 0) {
-        int dev = 0, cus = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            cus < 8)
-            cus = 256;
-        g = cus / 8 * 8;
-    }
-    return g;
+    const int cus = device_cu_count();
+    return cus < 8 ? 8 : cus / 8 * 8;
 }
 
 // PERSIST_OK = false: the caller only launches long reductions here, which
