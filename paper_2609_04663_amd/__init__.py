@@ -100,12 +100,17 @@ def _mat(t: torch.Tensor, dtype, name: str):
         raise TypeError(f"{name} must be a GPU tensor")
     if t.dtype != dtype:
         raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
-    if t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1) or t.stride(0) < max(1, t.shape[1]):
+    # the stride of a dimension of extent 1 is never used (NumPy-made tensors
+    # of shape (1, n) can carry a row stride of 1)
+    if (t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1)
+            or (t.shape[0] > 1 and t.stride(0) < max(1, t.shape[1]))):
         raise ValueError(f"{name} must be a row-major 2-D tensor with unit column stride")
     return t
 
 
 def _ld(t: torch.Tensor) -> int:
+    if t.shape[0] <= 1:
+        return max(1, t.shape[1])
     return max(1, t.stride(0), t.shape[1])
 
 

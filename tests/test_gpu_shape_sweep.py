@@ -201,3 +201,21 @@ def test_sgemm_tile_routes_within_bounds(emu, M, N, K, tile, splits):
     esc_cap = 2.0 ** -22 + (6 * 256 + math.ceil(K / 256)) * 2.0 ** -24
     assert np.all(err <= esc_cap * ab)
     assert np.sqrt(np.sum(err ** 2)) <= 4 * K * 2.0 ** -24 * np.sqrt(np.sum(hi ** 2))
+
+
+def test_single_row_operands_with_numpy_strides(emu):
+    """A (1, n) operand made from NumPy can carry a row stride of 1 (the
+    stride of an extent-1 dimension is arbitrary); the binding accepts it and
+    passes a leading dimension of n."""
+    K, N = 1519, 1
+    A = S.make("wide", 23001, (586, K), np.float64)
+    B = S.make("uniform", 23002, (K, N), np.float64)
+    Bt = np.ascontiguousarray(B.T)                 # shape (1, K), strides (8, 8)
+    tB = torch.from_numpy(Bt).cuda()
+    assert tB.shape == (1, K)
+    C = emu.dgemm_ex(dev(A), tB, 3, None, "N", "T").cpu().numpy()
+    ref, st = O.emu_dgemm(A, B, 3)
+    assert st == 0 and np.array_equal(C.view(np.uint64), ref.view(np.uint64))
+    row = torch.from_numpy(np.ascontiguousarray(S.make("normal", 23003, (K, 1), np.float32).T)).cuda()
+    Cs = emu.sgemm(row, dev(S.make("normal", 23004, (K, 7), np.float32))).cpu().numpy()
+    assert Cs.shape == (1, 7) and np.all(np.isfinite(Cs))
