@@ -4,7 +4,9 @@
  *
  * Problem (Sec. 3.2, Eq. gemm): C = A B with A (M x K), B (K x N), C (M x N),
  * all row-major with leading dimensions lda, ldb, ldc counted in elements.
- * There is no alpha/beta and no transpose: C is fully overwritten.
+ * emu_sgemm / emu_dgemm have no alpha/beta and no transpose: C is fully
+ * overwritten.  The BLAS forms emu_sgemm_ex / emu_dgemm_ex (below) add
+ * op(A), op(B) and C = alpha op(A) op(B) + beta C.
  *
  * Pointers.  A, B and C are device pointers (HIP global memory) owned by the
  * caller; A and B are only read.  C must not alias A or B.  Every call is
@@ -57,6 +59,14 @@ extern "C" {
 #define EMU_STATUS_SUBNORMAL 4u /* a nonzero component is subnormal in BF16 or
                                    underflowed (the split is not exact) */
 #define EMU_STATUS_OVERFLOW 8u  /* a component overflowed BF16 */
+#define EMU_STATUS_INEXACT 16u  /* (emu_dgemm) a retained panel product may leave
+                                   FP32's exact range: for some (i, j) of the
+                                   product set, 2^(vA_i + vB_j - 16) (the unit of
+                                   the panel sum) is below 2^-126 or
+                                   2^(vA_i + vB_j + 8) (its bound) above 2^127,
+                                   so that product may be rounded or overflow in
+                                   FP32 and the result is not Eq.
+                                   (fp64reconstruction) with exact panel products */
 
 /* FP64 split projection constant (Eq. fp64split).  SYM (default) uses
    Sigma = 0.75 * 2^(v+45): granularity 2^(v-8) for both signs, which is the
@@ -82,8 +92,11 @@ extern "C" {
 
 /* Emulated SGEMM, Algorithm fp32 (Sec. 4.2, Eq. fp32split and fp32six):
    each FP32 operand is split into three BF16 components; the six products
-   A_iB_j with i + j < 3 are evaluated with FP32 accumulation on bf16 MFMA and
-   combined in FP32 per reduction panel of 256.  A: M x K (lda), B: K x N
+   A_iB_j with i + j < 3 are evaluated with FP32 accumulation on bf16 MFMA.
+   The leading product A0B0 is accumulated per reduction panel of 256 and each
+   panel sum is added into an FP32 total; the five smaller products share a
+   second FP32 accumulator over the whole reduction (or over each part of a
+   split reduction), added to the total at the end.  A: M x K (lda), B: K x N
    (ldb), C: M x N (ldc), device pointers, FP32. */
 int emu_sgemm(int64_t M, int64_t N, int64_t K, const float *A, int64_t lda, const float *B,
               int64_t ldb, float *C, int64_t ldc);

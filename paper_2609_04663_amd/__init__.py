@@ -27,7 +27,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libemu.so")
 
 EMU_OK, EMU_EINVAL, EMU_EHIP, EMU_ENOMEM = 0, 1, 2, 3
-STATUS_NAN, STATUS_RANGE, STATUS_SUBNORMAL, STATUS_OVERFLOW = 1, 2, 4, 8
+STATUS_NAN, STATUS_RANGE, STATUS_SUBNORMAL, STATUS_OVERFLOW, STATUS_INEXACT = 1, 2, 4, 8, 16
 SPLIT_SYM, SPLIT_LITERAL = 0, 1
 SCOPE_OPERAND, SCOPE_ROWCOL = 0, 1
 # the paper's product counts N_p(d), d = 3 .. 6 (Eq. fp64productcounts) ...
@@ -95,9 +95,10 @@ def _bind_stream(dev: torch.device):
     lib().emu_set_stream(ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream))
 
 
-def _mat(t: torch.Tensor, dtype, name: str):
-    if not isinstance(t, torch.Tensor) or not t.is_cuda:
-        raise TypeError(f"{name} must be a GPU tensor")
+def _layout(t: torch.Tensor, dtype, name: str):
+    """dtype and row-major layout checks (metadata only, any device)."""
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
     if t.dtype != dtype:
         raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
     # the stride of a dimension of extent 1 is never used (NumPy-made tensors
@@ -108,6 +109,29 @@ def _mat(t: torch.Tensor, dtype, name: str):
     return t
 
 
+def _on_gpu(*named):
+    for name, t in named:
+        if not t.is_cuda:
+            raise TypeError(f"{name} must be a GPU tensor")
+
+
+def _mat(t: torch.Tensor, dtype, name: str):
+    _layout(t, dtype, name)
+    _on_gpu((name, t))
+    return t
+
+
+def _out(C, M: int, N: int, dtype, device):
+    """The output C: allocated when None, else checked to be M x N (the
+    library writes M rows of ldc elements: a smaller C would be overrun)."""
+    if C is None:
+        return torch.empty((M, N), dtype=dtype, device=device)
+    _layout(C, dtype, "C")
+    if tuple(C.shape) != (M, N):
+        raise ValueError(f"C must be {M} x {N}, got {tuple(C.shape)}")
+    return C
+
+
 def _ld(t: torch.Tensor) -> int:
     if t.shape[0] <= 1:
         return max(1, t.shape[1])
@@ -115,15 +139,14 @@ def _ld(t: torch.Tensor) -> int:
 
 
 def sgemm(A: torch.Tensor, B: torch.Tensor, C: torch.Tensor | None = None) -> torch.Tensor:
-    _mat(A, torch.float32, "A")
-    _mat(B, torch.float32, "B")
+    _layout(A, torch.float32, "A")
+    _layout(B, torch.float32, "B")
     M, K = A.shape
     K2, N = B.shape
     if K != K2:
         raise ValueError("inner dimensions differ")
-    if C is None:
-        C = torch.empty((M, N), dtype=torch.float32, device=A.device)
-    _mat(C, torch.float32, "C")
+    C = _out(C, M, N, torch.float32, A.device)
+    _on_gpu(("A", A), ("B", B), ("C", C))
     _bind_stream(A.device)
     _check(lib().emu_sgemm(M, N, K, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), C.data_ptr(),
                            _ld(C)))
@@ -132,15 +155,14 @@ def sgemm(A: torch.Tensor, B: torch.Tensor, C: torch.Tensor | None = None) -> to
 
 def dgemm(A: torch.Tensor, B: torch.Tensor, nprod: int,
           C: torch.Tensor | None = None) -> torch.Tensor:
-    _mat(A, torch.float64, "A")
-    _mat(B, torch.float64, "B")
+    _layout(A, torch.float64, "A")
+    _layout(B, torch.float64, "B")
     M, K = A.shape
     K2, N = B.shape
     if K != K2:
         raise ValueError("inner dimensions differ")
-    if C is None:
-        C = torch.empty((M, N), dtype=torch.float64, device=A.device)
-    _mat(C, torch.float64, "C")
+    C = _out(C, M, N, torch.float64, A.device)
+    _on_gpu(("A", A), ("B", B), ("C", C))
     _bind_stream(A.device)
     _check(lib().emu_dgemm(M, N, K, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), C.data_ptr(),
                            _ld(C), int(nprod)))
@@ -154,19 +176,16 @@ def _op_shape(X: torch.Tensor, trans: str):
 
 
 def _gemm_ex(fn, dtype, A, B, C, transa, transb, alpha, beta, extra=()):
-    _mat(A, dtype, "A")
-    _mat(B, dtype, "B")
+    _layout(A, dtype, "A")
+    _layout(B, dtype, "B")
     M, K = _op_shape(A, transa)
     K2, N = _op_shape(B, transb)
     if K != K2:
         raise ValueError("inner dimensions differ")
-    if C is None:
-        if beta != 0:
-            raise ValueError("beta != 0 needs C")
-        C = torch.empty((M, N), dtype=dtype, device=A.device)
-    _mat(C, dtype, "C")
-    if tuple(C.shape) != (M, N):
-        raise ValueError("C must be M x N")
+    if C is None and beta != 0:
+        raise ValueError("beta != 0 needs C")
+    C = _out(C, M, N, dtype, A.device)
+    _on_gpu(("A", A), ("B", B), ("C", C))
     _bind_stream(A.device)
     _check(fn(transa.encode(), transb.encode(), M, N, K, alpha, A.data_ptr(), _ld(A),
               B.data_ptr(), _ld(B), beta, C.data_ptr(), _ld(C), *extra))

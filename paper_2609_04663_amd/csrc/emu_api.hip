@@ -389,7 +389,7 @@ int emu_dgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, doub
     const F64SplitOperand ops[2] = {
         {A, ar, ac, lda, ta ? 1 : 0, scaled ? sc.sa : nullptr, Ap, s.RpadA, st},
         {B, br, bc, ldb, tb ? 0 : 1, scaled ? sc.sb : nullptr, Bp, s.RpadB, st + F64_SLOTS}};
-    e = launch_split_f64(ops, 2, s.KB, np, g_split_mode, ws_status(), g_stream);
+    e = launch_split_f64(ops, 2, s.KB, np, g_split_mode, d, ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f64");
     prof_mark(1);
     e = launch_gemm_f64(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, scaled ? sc.sa : nullptr,
@@ -452,7 +452,7 @@ int emu_split_f64(int64_t R, int64_t Cc, const double *X, int64_t ldx, int as_b,
     }
     const F64SplitOperand op = {X, R, Cc, ldx, as_b != 0 ? 1 : 0, scaled ? sc.sa : nullptr, P,
                                 s.RpadA, st};
-    e = launch_split_f64(&op, 1, s.KB, 6, g_split_mode, ws_status(), g_stream);
+    e = launch_split_f64(&op, 1, s.KB, 6, g_split_mode, 0, ws_status(), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f64");
     if (R > 0 && Cc > 0) {
         e = launch_unpack(P, 6, s.KB, s.RpadA, R, Cc, as_b != 0, slices, g_stream);

@@ -48,7 +48,7 @@ __host__ __device__ inline int64_t packed_index(int c, int64_t kb, int64_t row, 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
 // Status bits (same values as EMU_STATUS_* in emu.h).
-constexpr unsigned ST_NAN = 1u, ST_RANGE = 2u, ST_SUBNORMAL = 4u, ST_OVERFLOW = 8u;
+constexpr unsigned ST_NAN = 1u, ST_RANGE = 2u, ST_SUBNORMAL = 4u, ST_OVERFLOW = 8u, ST_INEXACT = 16u;
 
 // Device state of the FP64 split of one operand: the operand-wide per-level
 // maxima (bit patterns of non-negative doubles, whose unsigned order is the
@@ -103,9 +103,11 @@ hipError_t launch_scale_c_f64(double *C, int64_t M, int64_t N, int64_t ldc, doub
 hipError_t launch_split_f32(const F32SplitOperand *ops, int nops, int64_t KB, unsigned *status,
                             hipStream_t s);
 // The FP64 split of nops <= 2 operands with the same KB: nlev <= 6 levels
-// (planes) each, 2 + nlev launches in all.
+// (planes) each, 2 + nlev launches in all.  dcheck = d > 0 (with nops = 2, A
+// then B): also set ST_INEXACT when a product of S_d may leave FP32's exact
+// range.
 hipError_t launch_split_f64(const F64SplitOperand *ops, int nops, int64_t KB, int nlev, int mode,
-                            unsigned *status, hipStream_t s);
+                            int dcheck, unsigned *status, hipStream_t s);
 // per-row (by_col = 0) or per-column exponents ceil(log2 max|x|) of X; mb is
 // scratch of rows (or cols) 64-bit words
 hipError_t launch_scale_exponents(const double *X, int64_t rows, int64_t cols, int64_t ldx,

@@ -171,6 +171,8 @@ struct F64SplitArgs {
     int blocks0;          // blocks of operand 0; the rest serve operand 1
     int64_t KB;
     unsigned *status;
+    int dcheck;           // depth d of the product set to range-check (A = op 0,
+                          // B = op 1), or 0 for none
 };
 
 // The block's operand (selected, not indexed, so that the arguments stay in the
@@ -356,13 +358,12 @@ __device__ __forceinline__ void split_f64_pass(const F64SplitOperand op, int64_t
     }
 }
 
-__global__ __launch_bounds__(SPLIT_THREADS) void split_f64_kernel(F64SplitArgs a, int pass) {
-    int b, nb;
-    const F64SplitOperand &op = operand_of_block(a, b, nb);
-    const F64SplitState &in = op.st[pass];
-    F64SplitState *out = op.st + pass + 1;
-    const int nlev = in.nlev, step = in.mode ? 8 : 9;
-    int v[6];
+// The exponent chain pass `pass` uses, from the slot `in` the previous pass
+// wrote (slot 0, the level-0 maximum, for pass 0); returns the first level the
+// pass recomputes, or -1 once the chain is verified.  Pass p fixes level p for
+// good, so the chain of the last pass (nlev - 1) is final for levels < nlev.
+__device__ inline int chain_of(const F64SplitState &in, int pass, int step, int (&v)[6]) {
+    const int nlev = in.nlev;
     unsigned long long mb[6];
     int r0 = -1;
 #pragma unroll
@@ -373,42 +374,78 @@ __global__ __launch_bounds__(SPLIT_THREADS) void split_f64_kernel(F64SplitArgs a
         const int v0 = (m0 == 0.0) ? V_ZERO : ceil_log2_pos(m0);
 #pragma unroll
         for (int r = 0; r < 6; ++r) v[r] = (v0 == V_ZERO) ? V_ZERO : v0 - step * r;
-        r0 = 0;
-    } else {
-        // verify the levels after the previous pass's first recomputed level
-        // (compile-time level indices keep v and mb in registers)
-        const int rf = in.replay_from;
-        bool done = rf < 0;
-#pragma unroll
-        for (int r = 1; r < 6; ++r) {
-            if (done || r <= rf || r >= nlev) continue;
-            if (v[r - 1] == V_ZERO) { v[r] = V_ZERO; continue; }
-            const double m = __longlong_as_double((long long)mb[r]);
-            if (m == 0.0) {
-#pragma unroll
-                for (int t = r; t < 6; ++t) v[t] = V_ZERO;
-                done = true;
-                continue;
-            }
-            const int vt = ceil_log2_pos(m);
-            if (vt == v[r]) continue;
-            v[r] = vt;
-#pragma unroll
-            for (int t = r + 1; t < 6; ++t) v[t] = vt - step * (t - r);
-            r0 = r;
-            done = true;
-        }
+        return 0;
     }
+    // verify the levels after the previous pass's first recomputed level
+    // (compile-time level indices keep v and mb in registers)
+    const int rf = in.replay_from;
+    bool done = rf < 0;
+#pragma unroll
+    for (int r = 1; r < 6; ++r) {
+        if (done || r <= rf || r >= nlev) continue;
+        if (v[r - 1] == V_ZERO) { v[r] = V_ZERO; continue; }
+        const double m = __longlong_as_double((long long)mb[r]);
+        if (m == 0.0) {
+#pragma unroll
+            for (int t = r; t < 6; ++t) v[t] = V_ZERO;
+            done = true;
+            continue;
+        }
+        const int vt = ceil_log2_pos(m);
+        if (vt == v[r]) continue;
+        v[r] = vt;
+#pragma unroll
+        for (int t = r + 1; t < 6; ++t) v[t] = vt - step * (t - r);
+        r0 = r;
+        done = true;
+    }
+    return r0;
+}
+
+// Whether every retained panel product is an exact FP32 value for the final
+// chains vA, vB.  A slice entry is a multiple of 2^(v - 8) of magnitude at
+// most 2^v, so the panel sum of A_i B_j (256 terms) is a multiple of
+// u = 2^(vA_i + vB_j - 16) below 2^24 u.  Every partial sum is then a normal
+// FP32 value (or 0) when u >= 2^-126 and 2^24 u <= 2^127; outside that range
+// the FP32 accumulation may round or overflow.  Pairs with an all-zero slice
+// contribute exact zeros.
+__device__ inline bool panel_products_in_range(const int (&vA)[6], const int (&vB)[6], int d) {
+    bool ok = true;
+#pragma unroll
+    for (int i = 0; i < 6; ++i)
+#pragma unroll
+        for (int j = 0; j < 6; ++j) {
+            if (i + j >= d || vA[i] == V_ZERO || vB[j] == V_ZERO) continue;
+            const int e = vA[i] + vB[j];
+            if (e - 16 < -126 || e + 8 > 127) ok = false;
+        }
+    return ok;
+}
+
+__global__ __launch_bounds__(SPLIT_THREADS) void split_f64_kernel(F64SplitArgs a, int pass) {
+    int b, nb;
+    const F64SplitOperand &op = operand_of_block(a, b, nb);
+    const F64SplitState &in = op.st[pass];
+    F64SplitState *out = op.st + pass + 1;
+    const int nlev = in.nlev, step = in.mode ? 8 : 9;
+    int v[6];
+    const int r0 = chain_of(in, pass, step, v);
     if (b == 0 && threadIdx.x == 0) {
         // levels <= r0 keep their maxima (all of them once verified); the
         // levels after r0 are filled by this pass's atomics
         for (int r = 0; r < 6; ++r) {
             out->v[r] = v[r];
-            if (r0 < 0 || r <= r0) out->maxbits[r] = mb[r];
+            if (r0 < 0 || r <= r0) out->maxbits[r] = in.maxbits[r];
         }
         out->replay_from = r0;
         out->nlev = nlev;
         out->mode = in.mode;
+        // the last pass holds the final chains: range-check the products
+        if (a.dcheck > 0 && pass == nlev - 1 && a.nops == 2 && blockIdx.x == 0) {
+            int vb[6];
+            (void)chain_of(a.op[1].st[pass], pass, step, vb);
+            if (!panel_products_in_range(v, vb, a.dcheck)) atomicOr(a.status, ST_INEXACT);
+        }
     }
     if (r0 < 0) return;                                   // verified: nothing to redo
     const double cst = in.mode ? 1.0 : 0.75;
@@ -582,13 +619,15 @@ hipError_t launch_split_f32(const F32SplitOperand *ops, int nops, int64_t KB, un
 // Full FP64 split of the operands: init, level-0 maxima, then nlev passes (the
 // first speculative; each later one verifies, and replays only on a mismatch).
 hipError_t launch_split_f64(const F64SplitOperand *ops, int nops, int64_t KB, int nlev, int mode,
-                            unsigned *status, hipStream_t s) {
-    if (nops < 1 || nops > 2 || nlev < 1 || nlev > 6) return hipErrorInvalidValue;
+                            int dcheck, unsigned *status, hipStream_t s) {
+    if (nops < 1 || nops > 2 || nlev < 1 || nlev > 6 || (dcheck > 0 && nops != 2))
+        return hipErrorInvalidValue;
     F64SplitArgs a{};
     for (int o = 0; o < nops; ++o) a.op[o] = ops[o];
     a.nops = nops;
     a.KB = KB;
     a.status = status;
+    a.dcheck = dcheck;
     f64_state_init<<<1, 64, 0, s>>>(a, nlev, mode);
     // at most 512 blocks per operand: each ends in one atomic on the maximum
     auto max_blocks = [](int64_t rows) { return (int)(rows < 512 ? (rows > 0 ? rows : 1) : 512); };

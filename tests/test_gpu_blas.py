@@ -58,6 +58,40 @@ def test_sgemm_ex_transposes_give_the_plain_bits(emu, ta, tb, shape):
     assert np.array_equal(got.view(np.uint32), P.view(np.uint32))
 
 
+@pytest.mark.parametrize("ta,tb", CASES)
+@pytest.mark.parametrize("shape", SHAPES)
+def test_sgemm_ex_against_the_oracle(emu, ta, tb, shape):
+    """The SGEMM BLAS forms against the oracle's composition, at the bar of the
+    plain emulated SGEMM: against the exact value alpha (AB) + beta C (FP64
+    products of the FP32 inputs, double-double sums), the GPU's normwise error
+    is at most twice the oracle's (plus the FP32 rounding of the update, which
+    both pay), and each entry stays within the per-entry cap of the plain call
+    scaled by |alpha|, plus one rounding of the output."""
+    M, N, K = shape
+    A = S.make("normal", 751, (M, K), np.float32)
+    B = S.make("normal", 752, (K, N), np.float32)
+    C0 = S.make("normal", 753, (M, N), np.float32)
+    A64, B64 = A.astype(np.float64), B.astype(np.float64)
+    hi, lo = O.ref_gemm_dd(A64, B64)
+    absp = np.abs(A64) @ np.abs(B64)
+    _, esc_cap = sgemm_bounds(K)
+    for alpha, beta in ((1.0, 0.0), (-0.75, 0.5), (2.5, -1.25)):
+        ref = (alpha * hi + beta * C0.astype(np.float64)) + alpha * lo
+        orc, _ = O.emu_sgemm_ex(stored(A, ta), stored(B, tb), C0, ta, tb, alpha, beta)
+        got = emu.sgemm_ex(dev(stored(A, ta)), dev(stored(B, tb)), dev(C0.copy()), ta, tb,
+                           alpha, beta).cpu().numpy()
+        e_gpu, e_orc = O.e_F(got, ref), O.e_F(orc, ref)
+        assert e_gpu <= 2 * e_orc + 2.0 ** -24, (alpha, beta, e_gpu, e_orc)
+        err = np.abs(got.astype(np.float64) - ref)
+        cap = abs(alpha) * esc_cap * absp + 2.0 ** -23 * np.abs(ref)
+        assert np.all(err <= cap), (alpha, beta, float(np.max(err / np.maximum(cap, 1e-300))))
+
+
+def sgemm_bounds(K):
+    """The absolute caps of the plain emulated SGEMM (normwise, per entry)."""
+    return 4 * K * 2.0 ** -24, 2.0 ** -22 + (6 * 256 + -(-K // 256)) * 2.0 ** -24
+
+
 @pytest.mark.parametrize("alpha,beta", [(2.0, 0.0), (-0.5, 1.0), (1.5, -3.25)])
 def test_sgemm_ex_output_update_rounding(emu, alpha, beta):
     """The update on the GPU's own product P: fl(fl(alpha P) + fl(beta C))."""

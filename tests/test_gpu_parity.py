@@ -318,6 +318,40 @@ def test_dgemm_domain_status(emu):
     assert emu.domain_status() == 0
 
 
+def test_dgemm_inexact_status_for_tiny_operands(emu):
+    """Operands of magnitude 2^-45 are inside Eq. (bf16rangefp64) and their
+    six slices are normal BF16 values, yet the lower panel products of
+    nprod = 21 fall below FP32's normal range (unit 2^(vA_i + vB_j - 16) down
+    to 2^-151): the library reports EMU_STATUS_INEXACT, and the oracle, which
+    rounds each exact panel sum to FP32, finds inexact panels there.  At
+    nprod = 6 every unit is at least 2^-124: no flag, and the result is the
+    unscaled operands' result times 2^-90 bit for bit (powers of two commute
+    with every rounding of the method while nothing leaves the normal range)."""
+    A = S.make("uniform", 361, (70, 600), np.float64)
+    B = S.make("uniform", 362, (600, 50), np.float64)
+    As, Bs = np.ldexp(A, -45), np.ldexp(B, -45)
+    emu.domain_status()
+    C6 = emu.dgemm(dev(As), dev(Bs), 6).cpu().numpy()
+    assert emu.domain_status() == 0
+    ref6, st6 = O.emu_dgemm(As, Bs, 6)
+    assert st6 == 0 and np.array_equal(C6, ref6)
+    assert np.array_equal(C6, np.ldexp(emu.dgemm(dev(A), dev(B), 6).cpu().numpy(), -90))
+    emu.dgemm(dev(As), dev(Bs), 21)
+    assert emu.domain_status() == emu.STATUS_INEXACT
+    _, st21 = O.emu_dgemm(As, Bs, 21)
+    assert st21 == O.ST_INEXACT32
+
+
+def test_dgemm_inexact_status_for_fp32_overflow(emu):
+    """Operands near 2^64: the leading panel product's bound 2^(vA_0 + vB_0 + 8)
+    exceeds FP32's range, so the status is raised; the split itself is exact."""
+    A = np.ldexp(S.make("uniform", 363, (40, 300), np.float64), 64)
+    B = np.ldexp(S.make("uniform", 364, (300, 30), np.float64), 64)
+    emu.domain_status()
+    emu.dgemm(dev(A), dev(B), 6)
+    assert emu.domain_status() == emu.STATUS_INEXACT
+
+
 def test_workspace_limit_gives_enomem(emu):
     emu.release_workspace()
     os.environ["EMU_WORKSPACE_LIMIT"] = "4096"

@@ -134,3 +134,34 @@ def test_blas_forms_empty_output_and_nprod(L):
     assert L.emu_sgemm_ex(b"T", b"T", 0, 4, 4, 1.0, P, 1, P, 4, 0.0, P, 4) == emu.EMU_OK
     assert L.emu_dgemm_ex(b"n", b"t", 4, 0, 4, 1.0, P, 4, P, 4, 0.0, P, 1, 21) == emu.EMU_OK
     assert L.emu_dgemm_ex(b"N", b"N", 4, 4, 4, 1.0, P, 4, P, 4, 0.0, P, 4, 7) == emu.EMU_EINVAL
+
+
+@pytest.mark.parametrize("cshape", [(1, 6), (4, 6), (5, 5), (5, 7), (6, 6)])
+def test_binding_rejects_wrong_output_shape(cshape):
+    """A caller-supplied C must be M x N: the library writes M rows of ldc
+    entries and a smaller C would be overrun.  The binding checks shapes from
+    tensor metadata before any device work, so host tensors reach the check."""
+    import torch
+    import paper_2609_04663_amd as emu
+    M, N, K = 5, 6, 3
+    for dt, fn, extra in ((torch.float32, emu.sgemm, ()), (torch.float64, emu.dgemm, (6,))):
+        A = torch.zeros((M, K), dtype=dt)
+        B = torch.zeros((K, N), dtype=dt)
+        C = torch.zeros(cshape, dtype=dt)
+        with pytest.raises(ValueError, match="C must be"):
+            fn(A, B, *extra, C=C)
+    for dt, fn, extra in ((torch.float32, emu.sgemm_ex, ()), (torch.float64, emu.dgemm_ex, (6,))):
+        A = torch.zeros((K, M), dtype=dt)                 # stored transposed
+        B = torch.zeros((N, K), dtype=dt)
+        C = torch.zeros(cshape, dtype=dt)
+        with pytest.raises(ValueError, match="C must be"):
+            fn(A, B, *extra, C=C, transa="T", transb="T")
+
+
+def test_binding_needs_gpu_tensors_after_the_shape_checks():
+    import torch
+    import paper_2609_04663_amd as emu
+    A = torch.zeros((5, 3), dtype=torch.float64)
+    B = torch.zeros((3, 6), dtype=torch.float64)
+    with pytest.raises(TypeError, match="GPU tensor"):
+        emu.dgemm(A, B, 6, C=torch.zeros((5, 6), dtype=torch.float64))

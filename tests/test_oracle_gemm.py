@@ -322,3 +322,65 @@ def test_entries_match_full_gemm():
     assert np.array_equal(h2, hi[rows, cols]) and np.array_equal(l2, lo[rows, cols])
     ab = O.absprod_entries(A, B, rows, cols)
     assert np.allclose(ab, (np.abs(A) @ np.abs(B))[rows, cols], rtol=1e-14)
+
+
+# ---------------------------------------------------------------------------
+# the inexact-panel status bit (16): a panel product that is not an FP32 value
+
+
+def _inexact_by_definition(A, B, nprod, kc):
+    """Whether some exact panel sum of a retained product is not a binary32
+    value (Fractions over the oracle's own slices, which the split pins fix)."""
+    d = O.NPROD_TO_D[nprod]
+    sa, _, _, _ = O.split_f64(A)
+    sb, _, _, _ = O.split_f64(B)
+    M, K = A.shape
+    N = B.shape[1]
+    av = [[[bf16_value(sa[i, m, k]) for k in range(K)] for m in range(M)] for i in range(6)]
+    bv = [[[bf16_value(sb[j, k, n]) for k in range(K)] for n in range(N)] for j in range(6)]
+    for m in range(M):
+        for n in range(N):
+            for p0 in range(0, K, kc):
+                for ell in range(d):
+                    for i in range(max(0, ell - 5), min(ell, 5) + 1):
+                        j = ell - i
+                        P = sum(av[i][m][k] * bv[j][n][k] for k in range(p0, min(K, p0 + kc)))
+                        r = to_f32(P)
+                        if isinstance(r, float) or r != P:
+                            return True
+    return False
+
+
+def test_dgemm_inexact_panel_flag_long_panel():
+    """Slice entries of 255 units: 256 of them stay below 2^24 units (exact),
+    511 in one panel reach 511 * 255^2 > 2^24, an odd number of units that
+    binary32 cannot hold.  Panels of 512 must raise bit 16 and lose the exact
+    product; panels of 256 give it exactly with no flag."""
+    K = 511
+    A = np.full((2, K), 255.0 / 256.0)
+    B = np.full((K, 2), 255.0 / 256.0)
+    exact = Fraction(K) * Fraction(255, 256) ** 2
+    assert _inexact_by_definition(A, B, 6, 512) and not _inexact_by_definition(A, B, 6, 256)
+    C, st = O.emu_dgemm(A, B, 6, kc=512)
+    assert st & O.ST_INEXACT32 and Fraction(float(C[0, 0])) != exact
+    C, st = O.emu_dgemm(A, B, 6)
+    assert st == 0 and np.all(C == float(exact))
+
+
+@pytest.mark.parametrize("scale", [0, -30, -45])
+@pytest.mark.parametrize("nprod", [6, 15, 21])
+def test_dgemm_inexact_flag_matches_definition(scale, nprod):
+    """Tiny operands push the lower panel products below FP32's subnormal
+    spacing: the flag is raised exactly when some panel sum, computed with
+    exact rationals, is not a binary32 value."""
+    A = np.ldexp(S.make("uniform", 51, (2, 40), np.float64), scale)
+    B = np.ldexp(S.make("uniform", 52, (40, 2), np.float64), scale)
+    _, st = O.emu_dgemm(A, B, nprod)
+    assert bool(st & O.ST_INEXACT32) == _inexact_by_definition(A, B, nprod, 256)
+    assert (st & ~O.ST_INEXACT32) == 0
+
+
+def test_dgemm_inexact_flag_cases_are_not_vacuous():
+    A = np.ldexp(S.make("uniform", 51, (2, 40), np.float64), -45)
+    B = np.ldexp(S.make("uniform", 52, (40, 2), np.float64), -45)
+    assert _inexact_by_definition(A, B, 21, 256) and not _inexact_by_definition(A, B, 6, 256)

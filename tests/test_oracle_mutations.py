@@ -109,6 +109,11 @@ MUTATIONS = {
         "c = c1 | c2;",
         "c = c1;",
         [G.test_dot_bf16_f32_correct_rounding_wide_range]),
+    "inexact_panel_never_flagged": (
+        "    if (!isfinite(f)) return 0;\n    xacc d = *a;",
+        "    return 1;\n    xacc d = *a;",
+        [G.test_dgemm_inexact_panel_flag_long_panel,
+         lambda: G.test_dgemm_inexact_flag_matches_definition(-45, 21)]),
     "double_double_drops_product_error": (
         "c += pe + te;",
         "c += te;",
