@@ -117,6 +117,24 @@ int emu_sgemm(int64_t M, int64_t N, int64_t K, const float *A, int64_t lda, cons
 int emu_dgemm(int64_t M, int64_t N, int64_t K, const double *A, int64_t lda, const double *B,
               int64_t ldb, double *C, int64_t ldc, int nprod);
 
+/* emu_dgemm for callers that cannot allocate device memory: code under HIP
+   graph capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+   arguments, result and status reporting as emu_dgemm (current stream,
+   current split mode and scope), but it never allocates: instead of the
+   growing workspace it uses a fixed 64 MiB device array that the library
+   holds on every GPU it runs on until the process ends (its address is looked
+   up on the first call on each device, which also clears its status word with
+   a kernel).  A call whose packed planes (2 min(d, 6) bytes per element of
+   both operands, rows padded to whole tiles and K to whole k-blocks) plus a
+   2 KB header and, in the ROWCOL scope, 12 bytes per row of A and column of B
+   exceed 64 MiB returns EMU_ENOMEM before launching anything (about
+   M = N = K = 1600 at nprod >= 21, 2300 at nprod = 6).  All calls on one GPU
+   share that array: calls that overlap in time on one GPU (two streams, two
+   host threads) race and must be ordered by the caller.  C, A and B are the
+   caller's, as for emu_dgemm. */
+int emu_dgemm_noalloc(int64_t M, int64_t N, int64_t K, const double *A, int64_t lda,
+                      const double *B, int64_t ldb, double *C, int64_t ldc, int nprod);
+
 /* BLAS forms (the "more complete BLAS semantics" of Sec. 9):
      C = alpha op(A) op(B) + beta C,  row-major, op(X) = X or X^T.
    transa, transb: 'N' (op(X) = X) or 'T' ('C' is accepted as 'T'; lower case

@@ -39,7 +39,7 @@ EXPORTS = ("emu_sgemm", "emu_dgemm", "emu_set_stream", "emu_set_split_mode",
            "emu_domain_status", "emu_last_error", "emu_release_workspace",
            "emu_workspace_bytes", "emu_split_f32", "emu_split_f64", "emu_profile_enable",
            "emu_profile_read", "emu_set_split_scope", "emu_scale_exponents", "emu_sgemm_ex",
-           "emu_dgemm_ex")
+           "emu_dgemm_ex", "emu_dgemm_noalloc")
 
 
 class EmuError(RuntimeError):
@@ -62,6 +62,7 @@ def lib() -> ctypes.CDLL:
         i64, p, ci = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
         L.emu_sgemm.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64]
         L.emu_dgemm.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, ci]
+        L.emu_dgemm_noalloc.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, ci]
         L.emu_set_stream.argtypes = [p]
         L.emu_set_split_mode.argtypes = [ci]
         L.emu_set_split_scope.argtypes = [ci]
@@ -80,7 +81,7 @@ def lib() -> ctypes.CDLL:
                      "emu_domain_status", "emu_release_workspace", "emu_split_f32",
                      "emu_split_f64", "emu_profile_enable", "emu_profile_read",
                      "emu_set_split_scope", "emu_scale_exponents", "emu_sgemm_ex",
-                     "emu_dgemm_ex"):
+                     "emu_dgemm_ex", "emu_dgemm_noalloc"):
             getattr(L, name).restype = ci
         _lib = L
     return _lib
@@ -166,6 +167,25 @@ def dgemm(A: torch.Tensor, B: torch.Tensor, nprod: int,
     _bind_stream(A.device)
     _check(lib().emu_dgemm(M, N, K, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), C.data_ptr(),
                            _ld(C), int(nprod)))
+    return C
+
+
+def dgemm_noalloc(A: torch.Tensor, B: torch.Tensor, nprod: int, C: torch.Tensor) -> torch.Tensor:
+    """dgemm into a caller-supplied C without any device allocation by the
+    library (its fixed scratch; see emu_dgemm_noalloc in emu.h)."""
+    _layout(A, torch.float64, "A")
+    _layout(B, torch.float64, "B")
+    M, K = A.shape
+    K2, N = B.shape
+    if K != K2:
+        raise ValueError("inner dimensions differ")
+    if C is None:
+        raise ValueError("dgemm_noalloc needs C")
+    C = _out(C, M, N, torch.float64, A.device)
+    _on_gpu(("A", A), ("B", B), ("C", C))
+    _bind_stream(A.device)
+    _check(lib().emu_dgemm_noalloc(M, N, K, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B),
+                                   C.data_ptr(), _ld(C), int(nprod)))
     return C
 
 

@@ -29,6 +29,15 @@ int device_cu_count() {
 
 }  // namespace emu
 
+// Fixed scratch of the allocation-free entry point emu_dgemm_noalloc: header
+// (status word, split state), packed planes and scale-aware weights of one
+// call.  A file-scope device array: every GPU the library runs on holds its
+// own copy from the library's load until the process ends.  In host code the
+// name `scratch` only stands in for the symbol; the device address comes from
+// hipGetSymbolAddress, once per device, and only that address is used.
+constexpr size_t NOALLOC_BYTES = (size_t)64 << 20;
+static __device__ __align__(256) char scratch[NOALLOC_BYTES];
+
 namespace {
 
 using namespace emu;
@@ -123,9 +132,14 @@ void prof_mark(int p) {
     if (e && p == 2) ++g_prof.used;
 }
 
-unsigned *ws_status() { return reinterpret_cast<unsigned *>(g_ws.base); }
-F64SplitState *ws_states() { return reinterpret_cast<F64SplitState *>(g_ws.base + 128); }
-uint16_t *ws_planes(size_t off) { return reinterpret_cast<uint16_t *>(g_ws.base + HDR + off); }
+// Areas of a workspace (the growing one, or the fixed scratch of the
+// allocation-free entry point) starting at base.
+unsigned *ws_status(char *base) { return reinterpret_cast<unsigned *>(base); }
+F64SplitState *ws_states(char *base) { return reinterpret_cast<F64SplitState *>(base + 128); }
+uint16_t *ws_planes(char *base, size_t off) { return reinterpret_cast<uint16_t *>(base + HDR + off); }
+unsigned *ws_status() { return ws_status(g_ws.base); }
+F64SplitState *ws_states() { return ws_states(g_ws.base); }
+uint16_t *ws_planes(size_t off) { return ws_planes(g_ws.base, off); }
 
 // Scale-aware split scratch after the planes (256-byte aligned): 64-bit maxima
 // for the nA rows of A and the nB columns of B, then their int32 exponents.
@@ -134,13 +148,53 @@ struct ScaleArea {
     int *sa, *sb;             // [nA], [nB]
 };
 size_t scale_bytes(int64_t nA, int64_t nB) { return 256 + (size_t)(nA + nB) * 12; }
-ScaleArea ws_scales(size_t planes_bytes, int64_t nA, int64_t nB) {
+ScaleArea ws_scales(char *base, size_t planes_bytes, int64_t nA, int64_t nB) {
     const size_t off = (HDR + planes_bytes + 255) / 256 * 256;
     ScaleArea a;
-    a.mb = reinterpret_cast<unsigned long long *>(g_ws.base + off);
+    a.mb = reinterpret_cast<unsigned long long *>(base + off);
     a.sa = reinterpret_cast<int *>(a.mb + nA + nB);
     a.sb = a.sa + nA;
     return a;
+}
+ScaleArea ws_scales(size_t planes_bytes, int64_t nA, int64_t nB) {
+    return ws_scales(g_ws.base, planes_bytes, nA, nB);
+}
+
+// ---------------------------------------------------------------------------
+// The fixed scratch of emu_dgemm_noalloc (defined at file scope, above).
+constexpr int MAX_DEVICES = 64;
+char *g_scratch_ptr[MAX_DEVICES] = {};
+
+// The current device's scratch address (set up on the device's first call:
+// the symbol lookup and a clear of the status word, a kernel rather than a
+// memset so that a captured first call records nothing else), or null with
+// *rc set.
+char *scratch_for_current_device(int *rc) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+        *rc = hip_fail(e, "hipGetDevice");
+        return nullptr;
+    }
+    if (dev < 0 || dev >= MAX_DEVICES) {
+        *rc = fail(EMU_EINVAL, "device index beyond the allocation-free entry point's table");
+        return nullptr;
+    }
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr) {
+            *rc = hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol, "hipGetSymbolAddress(scratch)");
+            return nullptr;
+        }
+        e = launch_fill_f32(reinterpret_cast<float *>(ptr), 1, 1, 1, g_stream);
+        if (e != hipSuccess) {
+            *rc = hip_fail(e, "clear of the scratch status word");
+            return nullptr;
+        }
+        g_scratch_ptr[dev] = static_cast<char *>(ptr);
+    }
+    return g_scratch_ptr[dev];
 }
 
 // Depth d of the triangular selection S_d = {(i, j) : i, j < 6, i + j < d}
@@ -291,14 +345,24 @@ int emu_profile_read(int64_t cap, double *split_ms, double *gemm_ms, int64_t *ca
 int emu_domain_status(unsigned *flags) {
     if (!flags) return fail(EMU_EINVAL, "flags is NULL");
     *flags = 0;
-    if (!g_ws.base) return EMU_OK;
+    // the status words of the workspace and of the current device's scratch
+    int dev = 0;
+    char *words[2] = {g_ws.base, nullptr};
+    if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < MAX_DEVICES)
+        words[1] = g_scratch_ptr[dev];
+    if (!words[0] && !words[1]) return EMU_OK;
     hipError_t e = hipStreamSynchronize(g_stream);
     if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
-    e = hipMemcpy(flags, g_ws.base, sizeof(unsigned), hipMemcpyDeviceToHost);
-    if (e != hipSuccess) return hip_fail(e, "hipMemcpy(status)");
-    const unsigned zero = 0;
-    e = hipMemcpy(g_ws.base, &zero, sizeof(unsigned), hipMemcpyHostToDevice);
-    if (e != hipSuccess) return hip_fail(e, "hipMemcpy(status)");
+    for (char *w : words) {
+        if (!w) continue;
+        unsigned f = 0;
+        e = hipMemcpy(&f, w, sizeof(unsigned), hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpy(status)");
+        *flags |= f;
+        const unsigned zero = 0;
+        e = hipMemcpy(w, &zero, sizeof(unsigned), hipMemcpyHostToDevice);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpy(status)");
+    }
     return EMU_OK;
 }
 
@@ -347,32 +411,31 @@ int emu_sgemm(int64_t M, int64_t N, int64_t K, const float *A, int64_t lda, cons
     return emu_sgemm_ex('N', 'N', M, N, K, 1.0f, A, lda, B, ldb, 0.0f, C, ldc);
 }
 
-int emu_dgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, double alpha,
-                 const double *A, int64_t lda, const double *B, int64_t ldb, double beta,
-                 double *C, int64_t ldc, int nprod) {
-    const int d = nprod_to_d(nprod);
-    if (d < 0) return fail(EMU_EINVAL, "nprod must be 1, 3, 6, 10, 15, 21, 26, 30, 33, 35 or 36");
-    bool ta = false, tb = false;
-    int rc = trans_flag(transa, &ta);
-    if (!rc) rc = trans_flag(transb, &tb);
-    if (!rc) rc = check_gemm_args(ta, tb, M, N, K, A, lda, B, ldb, C, ldc, alpha != 0.0);
-    if (rc) return rc;
-    g_err.clear();
-    if (M == 0 || N == 0) return EMU_OK;
-    if (K == 0 || alpha == 0.0) {
-        hipError_t e = launch_scale_c_f64(C, M, N, ldc, beta, g_stream);
-        return e == hipSuccess ? EMU_OK : hip_fail(e, "scale C");
-    }
+}  // extern "C"
+
+namespace {
+
+// Bytes of workspace (after the header) an emulated DGEMM of depth d needs.
+size_t dgemm_ws_bytes(int64_t M, int64_t N, int64_t K, int d, bool scaled, Shape *sp) {
+    const Shape s = plan(M, N, K, dgemm_planes(d), dgemm_mt(d), DGEMM_NT);
+    if (sp) *sp = s;
+    return s.bytesA + s.bytesB + (scaled ? scale_bytes(M, N) : 0);
+}
+
+// The emulated DGEMM on a workspace at base (header, planes, weights), after
+// argument validation; M, N, K > 0 and alpha != 0.
+int dgemm_run(char *base, bool ta, bool tb, int64_t M, int64_t N, int64_t K, double alpha,
+              const double *A, int64_t lda, const double *B, int64_t ldb, double beta, double *C,
+              int64_t ldc, int d) {
     // Only the slices the retained products read are materialised; the levels
     // after them never influence the earlier slices.
     const int np = dgemm_planes(d);
-    const Shape s = plan(M, N, K, np, dgemm_mt(d), DGEMM_NT);
     const bool scaled = g_split_scope == EMU_SCOPE_ROWCOL;
-    rc = ensure_workspace(s.bytesA + s.bytesB + (scaled ? scale_bytes(M, N) : 0));
-    if (rc) return rc;
-    uint16_t *Ap = ws_planes(0), *Bp = ws_planes(s.bytesA);
-    F64SplitState *st = ws_states();
-    const ScaleArea sc = ws_scales(s.bytesA + s.bytesB, M, N);
+    Shape s;
+    (void)dgemm_ws_bytes(M, N, K, d, scaled, &s);
+    uint16_t *Ap = ws_planes(base, 0), *Bp = ws_planes(base, s.bytesA);
+    F64SplitState *st = ws_states(base);
+    const ScaleArea sc = ws_scales(base, s.bytesA + s.bytesB, M, N);
     // stored shapes: A is M x K ('N') or K x M ('T'); B is K x N ('N') or N x K ('T')
     const int64_t ar = ta ? K : M, ac = ta ? M : K, br = tb ? N : K, bc = tb ? K : N;
     prof_mark(0);
@@ -389,7 +452,7 @@ int emu_dgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, doub
     const F64SplitOperand ops[2] = {
         {A, ar, ac, lda, ta ? 1 : 0, scaled ? sc.sa : nullptr, Ap, s.RpadA, st},
         {B, br, bc, ldb, tb ? 0 : 1, scaled ? sc.sb : nullptr, Bp, s.RpadB, st + F64_SLOTS}};
-    e = launch_split_f64(ops, 2, s.KB, np, g_split_mode, d, ws_status(), g_stream);
+    e = launch_split_f64(ops, 2, s.KB, np, g_split_mode, d, ws_status(base), g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f64");
     prof_mark(1);
     e = launch_gemm_f64(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, scaled ? sc.sa : nullptr,
@@ -397,6 +460,66 @@ int emu_dgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, doub
     if (e != hipSuccess) return hip_fail(e, "gemm_f64");
     prof_mark(2);
     return EMU_OK;
+}
+
+// Validation and the degenerate cases of the DGEMM entry points; returns 1 when
+// dgemm_run must follow (d and the transposition flags set), else the result.
+int dgemm_prologue(char transa, char transb, int64_t M, int64_t N, int64_t K, double alpha,
+                   const double *A, int64_t lda, const double *B, int64_t ldb, double beta,
+                   double *C, int64_t ldc, int nprod, int *d, bool *ta, bool *tb, int *rc) {
+    *d = nprod_to_d(nprod);
+    if (*d < 0) {
+        *rc = fail(EMU_EINVAL, "nprod must be 1, 3, 6, 10, 15, 21, 26, 30, 33, 35 or 36");
+        return 0;
+    }
+    *rc = trans_flag(transa, ta);
+    if (!*rc) *rc = trans_flag(transb, tb);
+    if (!*rc) *rc = check_gemm_args(*ta, *tb, M, N, K, A, lda, B, ldb, C, ldc, alpha != 0.0);
+    if (*rc) return 0;
+    g_err.clear();
+    if (M == 0 || N == 0) return 0;
+    if (K == 0 || alpha == 0.0) {
+        hipError_t e = launch_scale_c_f64(C, M, N, ldc, beta, g_stream);
+        *rc = e == hipSuccess ? EMU_OK : hip_fail(e, "scale C");
+        return 0;
+    }
+    return 1;
+}
+
+}  // namespace
+
+extern "C" {
+
+int emu_dgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, double alpha,
+                 const double *A, int64_t lda, const double *B, int64_t ldb, double beta,
+                 double *C, int64_t ldc, int nprod) {
+    int d = 0, rc = EMU_OK;
+    bool ta = false, tb = false;
+    if (!dgemm_prologue(transa, transb, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, nprod, &d,
+                        &ta, &tb, &rc))
+        return rc;
+    rc = ensure_workspace(dgemm_ws_bytes(M, N, K, d, g_split_scope == EMU_SCOPE_ROWCOL, nullptr));
+    if (rc) return rc;
+    return dgemm_run(g_ws.base, ta, tb, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, d);
+}
+
+int emu_dgemm_noalloc(int64_t M, int64_t N, int64_t K, const double *A, int64_t lda,
+                      const double *B, int64_t ldb, double *C, int64_t ldc, int nprod) {
+    int d = 0, rc = EMU_OK;
+    bool ta = false, tb = false;
+    if (!dgemm_prologue('N', 'N', M, N, K, 1.0, A, lda, B, ldb, 0.0, C, ldc, nprod, &d, &ta, &tb,
+                        &rc))
+        return rc;
+    const size_t need =
+        HDR + dgemm_ws_bytes(M, N, K, d, g_split_scope == EMU_SCOPE_ROWCOL, nullptr);
+    if (need > NOALLOC_BYTES) {
+        g_err = "emu_dgemm_noalloc: this problem needs " + std::to_string(need) +
+                " bytes of scratch, more than the fixed " + std::to_string(NOALLOC_BYTES);
+        return EMU_ENOMEM;
+    }
+    char *base = scratch_for_current_device(&rc);
+    if (!base) return rc;
+    return dgemm_run(base, false, false, M, N, K, 1.0, A, lda, B, ldb, 0.0, C, ldc, d);
 }
 
 int emu_dgemm(int64_t M, int64_t N, int64_t K, const double *A, int64_t lda, const double *B,
