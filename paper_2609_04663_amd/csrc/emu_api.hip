@@ -237,7 +237,7 @@ struct Shape {
 
 // Packed sizes: rows padded to whole GEMM tiles (tile_m, tile_n are multiples
 // of ROW_GROUP), reduction padded to whole k-blocks.
-Shape plan(int64_t M, int64_t N, int64_t K, int nplanes, int tile_m, int tile_n) {
+Shape plan(int64_t M, int64_t N, int64_t K, int nplanes, int64_t tile_m, int64_t tile_n) {
     Shape s;
     s.KB = (K + KBLK - 1) / KBLK;
     s.RpadA = round_up(M, tile_m);
@@ -417,7 +417,12 @@ namespace {
 
 // Bytes of workspace (after the header) an emulated DGEMM of depth d needs.
 size_t dgemm_ws_bytes(int64_t M, int64_t N, int64_t K, int d, bool scaled, Shape *sp) {
-    const Shape s = plan(M, N, K, dgemm_planes(d), dgemm_mt(d), DGEMM_NT);
+    // the DGEMM kernel's tile rows and k-block multiple (padding is zero)
+    const int64_t KB = (K + KBLK - 1) / KBLK;
+    Shape s = plan(M, N, K, dgemm_planes(d), dgemm_tile_rows(d, M, N, KB), DGEMM_NT);
+    s.KB = dgemm_kb_padded(d, M, N, KB);
+    s.bytesA = (size_t)dgemm_planes(d) * s.KB * s.RpadA * KBLK * 2;
+    s.bytesB = (size_t)dgemm_planes(d) * s.KB * s.RpadB * KBLK * 2;
     if (sp) *sp = s;
     return s.bytesA + s.bytesB + (scaled ? scale_bytes(M, N) : 0);
 }

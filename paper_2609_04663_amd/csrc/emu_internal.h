@@ -33,7 +33,6 @@ constexpr int KPANEL = 256;     // reduction panel B_K of the FP32/FP64 reconstr
 // ... and of the GEMM tile that reads them (output tile rows for A, columns for B).
 constexpr int SGEMM_NT = 128;   // SGEMM output tiles: (192 or 128) x 128
 constexpr int DGEMM_NT = 64;
-inline int dgemm_mt(int d) { return d == 1 ? 256 : d <= 3 ? 128 : 64; }
 // Slices of each operand that the products of depth d read (indices < 6).
 inline int dgemm_planes(int d) { return d < 6 ? d : 6; }
 constexpr int KB_PER_PANEL = KPANEL / KBLK;
@@ -126,6 +125,12 @@ int sgemm_splits(int64_t M, int64_t N, int64_t KB, int tile_m);
 hipError_t launch_gemm_f32(const uint16_t *Ap, const uint16_t *Bp, float *C, int64_t M, int64_t N,
                            int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc, float alpha,
                            float beta, int tile_m, int splits, float *part, hipStream_t s);
+// Packed layout of a depth-d DGEMM (M x N output, KB k-blocks of data) for the
+// kernel that will run it: A's rows are padded to a multiple of
+// dgemm_tile_rows (B's columns to DGEMM_NT), and the reduction to
+// dgemm_kb_padded k-blocks (some kernels run whole panels; the padding is zero).
+int64_t dgemm_tile_rows(int d, int64_t M, int64_t N, int64_t KB);
+int64_t dgemm_kb_padded(int d, int64_t M, int64_t N, int64_t KB);
 // sa, sb: row weights of A and column weights of B to restore (C_mn times
 // 2^(sa_m + sb_n)), or both null
 hipError_t launch_gemm_f64(const uint16_t *Ap, const uint16_t *Bp, double *C, int64_t M,

@@ -614,6 +614,302 @@ __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
+// ---------------------------------------------------------------------------
+// Long reductions of depths d = 3 .. 6 on the 32 x 32 x 16 MFMA with wave tiles
+// of BM 32 x 32 blocks: four waves in a 2 x 2 grid, output tile (64 BM) x 64
+// (d = 6 and 5: BM = 1; d = 4: BM = 2; d = 3: BM = 3).  Every retained product's
+// accumulators (16 registers per block) stay live for the whole panel: the
+// first 16 sets in AGPRs, the rest in VGPRs through inline asm; the FP64 tile
+// (16 BM doubles per lane) is in VGPRs.  The operand fragments of a 16-index
+// sub-step (BM blocks of every A slice, one block of every B slice) are held in
+// one register set: each is re-read for the next sub-step right after its last
+// MFMA in the current one, except those whose last use comes too late for the
+// read to land in time (the double-buffered set of t_db), which are read into a
+// second buffer at the start of the sub-step.  The two sub-steps of a k-block
+// run the products in two orders chosen for that: sub-step 0 walks B's slices
+// downward (the A fragments finish late: they are the double-buffered ones),
+// sub-step 1 walks A's slices upward.  The k-block's d planes of both operands
+// are copied in 1 KB copies, d (BM + 1) per wave, NS k-blocks ahead through a
+// ring of NS LDS stages; one barrier per k-block, between its sub-steps.
+
+// Fragment codes: A slice i, block b -> 8 b + i (< 32); B slice j -> 32 + j.
+constexpr int fa_code(int i, int b) { return 8 * b + i; }
+constexpr int fb_code(int j) { return 32 + j; }
+// MFMA t of sub-step order o: code 64 b + 8 i + j (product A_i B_j on block b).
+template <int D, int BM>
+constexpr int t_mfma(int o, int t) {
+    const int npl = D < 6 ? D : 6;
+    int n = 0;
+    if (o == 1) {
+        for (int i = 0; i < npl; ++i)
+            for (int b = 0; b < BM; ++b)
+                for (int j = 0; j < npl; ++j)
+                    if (i + j < D && n++ == t) return 64 * b + 8 * i + j;
+    } else {
+        for (int j = npl - 1; j >= 0; --j)
+            for (int i = 0; i < npl; ++i)
+                for (int b = 0; b < BM; ++b)
+                    if (i + j < D && n++ == t) return 64 * b + 8 * i + j;
+    }
+    return -1;
+}
+template <int D, int BM>
+constexpr bool t_uses(int o, int t, int f) {
+    const int c = t_mfma<D, BM>(o, t);
+    const int b = c >> 6, i = (c >> 3) & 7, j = c & 7;
+    return f < 32 ? f == fa_code(i, b) : f == fb_code(j);
+}
+template <int D, int BM>
+constexpr int t_last(int o, int f) {
+    int l = -1;
+    for (int t = 0; t < n_prod(D) * BM; ++t)
+        if (t_uses<D, BM>(o, t, f)) l = t;
+    return l;
+}
+template <int D, int BM>
+constexpr int t_first(int o, int f) {
+    for (int t = 0; t < n_prod(D) * BM; ++t)
+        if (t_uses<D, BM>(o, t, f)) return t;
+    return -1;
+}
+template <int D, int BM>
+constexpr bool t_valid(int f) {
+    const int npl = D < 6 ? D : 6;
+    return f < 32 ? (f % 8 < npl && f / 8 < BM) : f - 32 < npl;
+}
+// Double-buffered: its last use in sub-step 0 falls in the last W0 MFMAs (the
+// read would still be in flight at the barrier that follows), or its last use
+// in sub-step 1 in the last W1 (the compiler waits for every outstanding LDS
+// read before the first MFMA of a k-block, since the k-block's copies count as
+// such events too), or fewer than four MFMAs separate its last use in sub-step
+// 1 from its first use in the next sub-step 0.
+template <int D, int BM, int W0, int W1>
+constexpr bool t_db(int f) {
+    const int T = n_prod(D) * BM;
+    return t_last<D, BM>(0, f) >= T - W0 || t_last<D, BM>(1, f) >= T - W1 ||
+           (T - 1 - t_last<D, BM>(1, f)) + t_first<D, BM>(0, f) < 4;
+}
+template <int D, int BM, int W0, int W1>
+constexpr int t_db_rank(int f) {
+    int r = 0;
+    for (int g = 0; g < f; ++g)
+        if (t_valid<D, BM>(g) && t_db<D, BM, W0, W1>(g)) ++r;
+    return r;
+}
+// Slot after whose MFMA fragment f is read for the next sub-step (order o).
+template <int D, int BM, int W0, int W1>
+constexpr int t_read_slot(int o, int f) {
+    return t_db<D, BM, W0, W1>(f) ? t_db_rank<D, BM, W0, W1>(f) : t_last<D, BM>(o, f);
+}
+// Product index q of pair (i, j) for d <= 6: diagonal l = i + j ascending, i ascending.
+constexpr int q_of(int i, int j) { return (i + j) * (i + j + 1) / 2 + i; }
+
+template <int D, int BM>
+struct CfgT {
+    static constexpr int P = n_prod(D);
+    static constexpr int NPL = D;                                   // d <= 6
+    static constexpr int MT = 64 * BM, NT = 64;
+    static constexpr int A_BYTES = MT * 64, B_BYTES = NT * 64;      // one plane of a stage
+    static constexpr int STAGE = NPL * (A_BYTES + B_BYTES);
+    static constexpr int NS = 160 * 1024 / STAGE < 4 ? 160 * 1024 / STAGE : 4;
+    static constexpr int COPIES = NPL * (BM + 1);                   // per wave and k-block
+    static constexpr int T = P * BM;                                // MFMAs per sub-step
+    static constexpr int Q_VGPR = T > 16 ? 16 / BM : P;             // AGPRs hold 16 sets
+    static_assert(D >= 3 && D <= 6, "depths 3 .. 6");
+    static_assert(4 * COPIES * 1024 == STAGE, "copy split");
+    static_assert(NS >= 3 && (NS - 1) * COPIES <= 63, "LDS stages");
+};
+
+template <int D, int BM, int W0, int W1>
+__global__ __launch_bounds__(256, 1) void gemm_f64t_kernel(
+    const uint16_t *__restrict__ Ap, const uint16_t *__restrict__ Bp, double *__restrict__ C,
+    int64_t M, int64_t N, int KB, int64_t RpadA, int64_t RpadB, int64_t ldc,
+    const int *__restrict__ sa, const int *__restrict__ sb, double alpha, double beta, int nt_m,
+    int nt_n) {
+    using K = CfgT<D, BM>;
+    constexpr int P = K::P, NPL = K::NPL, NS = K::NS, T = K::T;
+    __shared__ __attribute__((aligned(1024))) char lds[NS * K::STAGE];
+
+    int tm, tn;
+    tile_coords<8>(nt_m, nt_n, tm, tn);
+    const int lane = threadIdx.x & 63;
+    const unsigned lane16 = (unsigned)lane * 16u;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wm = wave >> 1, wn = wave & 1;
+    const int64_t m0 = (int64_t)tm * K::MT, n0 = (int64_t)tn * K::NT;
+
+    // Copy c of a k-block by wave w: for c < NPL BM, part 4 (c % BM) + w (16
+    // rows, 1 KB) of A plane c / BM; else part w of B plane c - NPL BM.  ak, bk:
+    // the copied k-block's slab of plane 0 at the tile's first row / column.
+    const char *Ag = reinterpret_cast<const char *>(Ap) + m0 * 64 + wave * 1024;
+    const char *Bg = reinterpret_cast<const char *>(Bp) + n0 * 64 + wave * 1024;
+    const int64_t a_plane = (int64_t)KB * RpadA * 64, b_plane = (int64_t)KB * RpadB * 64;
+    const int64_t a_kstep = RpadA * 64, b_kstep = RpadB * 64;
+    auto issue = [&](const char *ak, const char *bk, char *dst, auto c_c) {
+        constexpr int c = decltype(c_c)::value;
+        if constexpr (c < NPL * BM)
+            copy_1k(ak + (c / BM) * a_plane + (c % BM) * 4096,
+                    dst + (c / BM) * K::A_BYTES + (c % BM) * 4096 + wave * 1024, lane16);
+        else
+            copy_1k(bk + (c - NPL * BM) * b_plane,
+                    dst + NPL * K::A_BYTES + (c - NPL * BM) * K::B_BYTES + wave * 1024, lane16);
+    };
+    // copy cursor: the k-block whose copies are issued next (it stays on the
+    // last k-block once past it: in bounds, unused) and its stage
+    int c_kb = 0, c_st = 0;
+    const char *c_ak = Ag, *c_bk = Bg;
+    auto cursor_next = [&]() {
+        if (c_kb + 1 < KB) {
+            ++c_kb;
+            c_ak += a_kstep;
+            c_bk += b_kstep;
+        }
+        c_st = c_st + 1 == NS ? 0 : c_st + 1;
+    };
+    auto stage = [&](int s) -> char * { return lds + s * K::STAGE; };
+
+    const int off0 = frag_offset(lane, 0), off1 = frag_offset(lane, 1);
+    const char *const At0 = lds + (wm * 32 * BM) * 64;
+    const char *const Bt0 = lds + NPL * K::A_BYTES + (wn * 32) * 64;
+    // fragments: [slice][block][buffer]; buffer 1 only for the double-buffered ones
+    bf16x8 fa[NPL][BM][2], fb[NPL][2];
+    auto read_frag = [&](int so, int off, auto f_c, auto buf_c) {
+        constexpr int f = decltype(f_c)::value, u = decltype(buf_c)::value;
+        if constexpr (f < 32)
+            fa[f % 8][f / 8][u] = lds_frag(At0 + so + (f % 8) * K::A_BYTES + (f / 8) * 32 * 64, off);
+        else
+            fb[f - 32][u] = lds_frag(Bt0 + so + (f - 32) * K::B_BYTES, off);
+    };
+
+    f32x16 acc[P * BM];   // product q, block b at q BM + b
+    // Sub-step of order O (= its parity): the T MFMAs, the reads of the next
+    // sub-step (stage offset nso, lane offset noff) and NC copies of the
+    // cursor's k-block spread over the slots.  MFMA first in every slot: its
+    // operands were read a sub-step earlier.
+    auto step = [&](auto o_c, auto zero_c, int nso, int noff, auto nc_c) {
+        constexpr int O = decltype(o_c)::value;
+        constexpr bool zero = decltype(zero_c)::value;
+        constexpr int NC = decltype(nc_c)::value;
+        char *cdst = stage(c_st);
+        static_for<T>([&](auto t_c) {
+            constexpr int t = decltype(t_c)::value;
+            constexpr int code = t_mfma<D, BM>(O, t), b = code >> 6, i = (code >> 3) & 7,
+                          j = code & 7, x = q_of(i, j) * BM + b;
+            constexpr int ua = t_db<D, BM, W0, W1>(fa_code(i, b)) ? O : 0;
+            constexpr int ub = t_db<D, BM, W0, W1>(fb_code(j)) ? O : 0;
+            if constexpr (q_of(i, j) >= K::Q_VGPR) {
+                if constexpr (zero) mfma_vacc_zero(acc[x], fa[i][b][ua], fb[j][ub]);
+                else mfma_vacc(acc[x], fa[i][b][ua], fb[j][ub]);
+            } else {
+                acc[x] = mfma(fa[i][b][ua], fb[j][ub], zero ? f32x16{} : acc[x]);
+            }
+            order_fence();
+            static_for<40>([&](auto f_c) {
+                constexpr int f = decltype(f_c)::value;
+                if constexpr (t_valid<D, BM>(f) && t_read_slot<D, BM, W0, W1>(O, f) == t)
+                    read_frag(nso, noff, f_c,
+                              std::integral_constant<int, t_db<D, BM, W0, W1>(f) ? 1 - O : 0>{});
+            });
+            order_fence();
+            // NC copies spread over the T slots (the k-th after slot ceil((k + 1) T / NC) - 1)
+            if constexpr (NC > 0 && (t * NC) / T != ((t + 1) * NC) / T)
+                issue(c_ak, c_bk, cdst, std::integral_constant<int, (t * NC) / T>{});
+            order_fence();
+        });
+    };
+
+    // prologue: k-blocks 0 .. NS - 1 into the stages; wait for k-block 0
+    for (int s = 0; s < NS; ++s) {
+        static_for<K::COPIES>([&](auto c_c) { issue(c_ak, c_bk, stage(c_st), c_c); });
+        cursor_next();
+    }
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NS - 1) * K::COPIES) : "memory");
+    __syncthreads();
+    static_for<40>([&](auto f_c) {
+        if constexpr (t_valid<D, BM>(decltype(f_c)::value))
+            read_frag(0, off0, f_c, std::integral_constant<int, 0>{});
+    });
+
+    double acc64[BM][16];
+#pragma unroll
+    for (int b = 0; b < BM; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc64[b][r] = 0.0;
+
+    int qs = 0;   // stage of the current k-block
+    // k-block kb: sub-step 0, wait + barrier, sub-step 1 with the copies of
+    // k-block kb + NS (into the stage of kb, which no wave reads any more)
+    auto kblock = [&](auto zero_c) {
+        const int qn = qs + 1 == NS ? 0 : qs + 1;
+        step(std::integral_constant<int, 0>{}, zero_c, qs * K::STAGE, off1,
+             std::integral_constant<int, 0>{});
+        __builtin_amdgcn_sched_barrier(0);
+        // k-block kb + 1 landed: only kb + 2 .. kb + NS - 1 may still be in flight
+        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"((NS - 2) * K::COPIES) : "memory");
+        pipeline_barrier();
+        step(std::integral_constant<int, 1>{}, std::false_type{}, qn * K::STAGE, off0,
+             std::integral_constant<int, K::COPIES>{});
+        __builtin_amdgcn_sched_barrier(0);
+        cursor_next();
+        qs = qn;
+    };
+    // whole panels (KB is a multiple of 8: the planes are zero-padded to whole
+    // panels, which adds exact zeros to the last panel's sums); the panel's
+    // k-blocks are unrolled (a loop over them made the compiler spill the FP64
+    // tile around it)
+    for (int p0 = 0; p0 < KB; p0 += KB_PER_PANEL) {
+        kblock(std::true_type{});
+#pragma unroll
+        for (int kb = 1; kb < KB_PER_PANEL; ++kb) kblock(std::false_type{});
+        // panel end: widen each product exactly and add it in FP64, in order
+        // (one product at a time, so that only its values are in flight)
+#pragma unroll
+        for (int x = K::Q_VGPR * BM; x < P * BM; ++x) mfma_vacc_settle(acc[x]);
+        static_for<P>([&](auto q_c) {
+            constexpr int q = decltype(q_c)::value;
+#pragma unroll
+            for (int b = 0; b < BM; ++b)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc64[b][r] += (double)acc[q * BM + b][r];
+            __builtin_amdgcn_sched_barrier(0);
+        });
+    }
+    // the last trips issued (unused) copies: let them land before the
+    // workgroup ends and its LDS is handed to another workgroup
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+    const int64_t col = n0 + wn * 32 + (lane & 31);
+    const int col_w = (sa != nullptr && col < N) ? sb[col] : 0;
+#pragma unroll
+    for (int b = 0; b < BM; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int64_t row = m0 + wm * 32 * BM + b * 32 + acc_row(lane, r);
+            if (row < M && col < N) {
+                double val = acc64[b][r];
+                if (sa != nullptr) val = ldexp(val, sa[row] + col_w);
+                C[row * ldc + col] = out_update(val, alpha, beta, C + row * ldc + col);
+            }
+        }
+}
+
+// Blocks per wave of the long-reduction kernel at depth d (0: not used).
+constexpr int t_bm(int d) { return d == 6 || d == 5 ? 1 : d == 4 ? 2 : d == 3 ? 3 : 0; }
+
+template <int D, int W0 = 4, int W1 = 8>
+hipError_t launch_t64(const uint16_t *Ap, const uint16_t *Bp, double *C, int64_t M, int64_t N,
+                      int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc, const int *sa,
+                      const int *sb, double alpha, double beta, hipStream_t s) {
+    constexpr int BM = t_bm(D);
+    using K = CfgT<D, BM>;
+    if (KB % KB_PER_PANEL != 0 || RpadA % K::MT != 0 || RpadB % K::NT != 0)
+        return hipErrorInvalidValue;
+    const int nt_m = (int)((M + K::MT - 1) / K::MT), nt_n = (int)((N + K::NT - 1) / K::NT);
+    gemm_f64t_kernel<D, BM, W0, W1><<<nt_m * nt_n, 256, 0, s>>>(
+        Ap, Bp, C, M, N, (int)KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, nt_m, nt_n);
+    return hipGetLastError();
+}
+
 // Persistent grid of the DGEMM kernels: one workgroup per CU (their LDS use
 // allows one), rounded down to a multiple of 8.
 int persistent_workgroups() {
@@ -675,6 +971,30 @@ hipError_t launch_t(const uint16_t *Ap, const uint16_t *Bp, double *C, int64_t M
 
 }  // namespace
 
+namespace {
+// Depths whose long reductions run on gemm_f64t_kernel (whole panels).
+constexpr bool T_DEPTH[12] = {false, false, false, true, true, true, true,
+                              false, false, false, false, false};
+
+// Whether a depth-d DGEMM of an M x N output with KB k-blocks runs on
+// gemm_f64t_kernel: long reductions (K > 1024) whose (64 BM) x 64 tiles fill
+// the CUs (smaller grids keep the kernels with smaller tiles).
+bool use_t64(int d, int64_t M, int64_t N, int64_t KB) {
+    if (d < 3 || d > 6 || !T_DEPTH[d] || KB <= 32) return false;
+    const int64_t mt = 64 * t_bm(d);
+    return ((M + mt - 1) / mt) * ((N + DGEMM_NT - 1) / DGEMM_NT) >= persistent_workgroups();
+}
+}  // namespace
+
+int64_t dgemm_tile_rows(int d, int64_t M, int64_t N, int64_t KB) {
+    if (use_t64(d, M, N, KB)) return 64 * t_bm(d);
+    return d == 1 ? 256 : d <= 3 ? 128 : 64;   // a multiple of every other kernel's tile
+}
+
+int64_t dgemm_kb_padded(int d, int64_t M, int64_t N, int64_t KB) {
+    return use_t64(d, M, N, KB) ? (KB + KB_PER_PANEL - 1) / KB_PER_PANEL * KB_PER_PANEL : KB;
+}
+
 hipError_t launch_gemm_f64(const uint16_t *Ap, const uint16_t *Bp, double *C, int64_t M,
                            int64_t N, int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc,
                            const int *sa, const int *sb, double alpha, double beta, int d,
@@ -692,6 +1012,15 @@ hipError_t launch_gemm_f64(const uint16_t *Ap, const uint16_t *Bp, double *C, in
         return ((M + mt - 1) / mt) * ((N + DGEMM_NT - 1) / DGEMM_NT) < pw;
     };
     const bool long_k = KB > 32;
+    if (use_t64(d, M, N, KB)) {
+        switch (d) {
+            case 3: return launch_t64<3>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
+            case 4: return launch_t64<4>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
+            case 5: return launch_t64<5>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
+            case 6: return launch_t64<6>(Ap, Bp, C, M, N, KB, RpadA, RpadB, ldc, sa, sb, alpha, beta, s);
+            default: return hipErrorInvalidValue;
+        }
+    }
     switch (d) {
         case 1:
             if (few_tiles(256))
