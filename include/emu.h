@@ -127,8 +127,8 @@ int emu_dgemm(int64_t M, int64_t N, int64_t K, const double *A, int64_t lda, con
    a kernel).  A call whose packed planes (2 min(d, 6) bytes per element of
    both operands, rows padded to whole tiles and K to whole k-blocks) plus a
    2 KB header and, in the ROWCOL scope, 12 bytes per row of A and column of B
-   exceed 64 MiB returns EMU_ENOMEM before launching anything (about
-   M = N = K = 1600 at nprod >= 21, 2300 at nprod = 6).  All calls on one GPU
+   exceed 64 MiB returns EMU_ENOMEM before launching anything (square
+   problems up to about M = N = K = 1500 at nprod = 21, 2100 at nprod = 6).  All calls on one GPU
    share that array: calls that overlap in time on one GPU (two streams, two
    host threads) race and must be ordered by the caller.  C, A and B are the
    caller's, as for emu_dgemm. */

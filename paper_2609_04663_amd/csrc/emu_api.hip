@@ -237,13 +237,14 @@ struct Shape {
 
 // Packed sizes: rows padded to whole GEMM tiles (tile_m, tile_n are multiples
 // of ROW_GROUP), reduction padded to whole k-blocks.
-Shape plan(int64_t M, int64_t N, int64_t K, int nplanes, int64_t tile_m, int64_t tile_n) {
+Shape plan(int64_t M, int64_t N, int64_t K, int nplanes, int64_t tile_m, int64_t tile_n,
+           int64_t KB = 0) {
     Shape s;
-    s.KB = (K + KBLK - 1) / KBLK;
-    s.RpadA = round_up(M, tile_m);
-    s.RpadB = round_up(N, tile_n);
-    s.bytesA = (size_t)nplanes * s.KB * s.RpadA * KBLK * 2;
-    s.bytesB = (size_t)nplanes * s.KB * s.RpadB * KBLK * 2;
+    s.KB = KB > 0 ? KB : (K + KBLK - 1) / KBLK;
+    s.RpadA = round_up(M, tile_m) + ROW_SKEW_TILES * tile_m;
+    s.RpadB = round_up(N, tile_n) + ROW_SKEW_TILES * tile_n;
+    s.bytesA = (size_t)nplanes * plane_elems(s.KB, s.RpadA) * 2;
+    s.bytesB = (size_t)nplanes * plane_elems(s.KB, s.RpadB) * 2;
     return s;
 }
 
@@ -419,10 +420,8 @@ namespace {
 size_t dgemm_ws_bytes(int64_t M, int64_t N, int64_t K, int d, bool scaled, Shape *sp) {
     // the DGEMM kernel's tile rows and k-block multiple (padding is zero)
     const int64_t KB = (K + KBLK - 1) / KBLK;
-    Shape s = plan(M, N, K, dgemm_planes(d), dgemm_tile_rows(d, M, N, KB), DGEMM_NT);
-    s.KB = dgemm_kb_padded(d, M, N, KB);
-    s.bytesA = (size_t)dgemm_planes(d) * s.KB * s.RpadA * KBLK * 2;
-    s.bytesB = (size_t)dgemm_planes(d) * s.KB * s.RpadB * KBLK * 2;
+    const Shape s = plan(M, N, K, dgemm_planes(d), dgemm_tile_rows(d, M, N, KB), DGEMM_NT,
+                         dgemm_kb_padded(d, M, N, KB));
     if (sp) *sp = s;
     return s.bytesA + s.bytesB + (scaled ? scale_bytes(M, N) : 0);
 }

@@ -6,10 +6,11 @@
 // B's columns, i.e. B is stored transposed so that every row is K-contiguous.
 //
 //   element (c, row, k) of component plane c lives at bf16 index
-//     ((c * KB + kb) * Rpad + row) * 32 + 8 * (q ^ swz(row)) + (k % 8)
+//     c * plane_elems(KB, Rpad) + (kb * Rpad + row) * 32 + 8 * (q ^ swz(row)) + (k % 8)
 //   with kb = k / 32, q = (k % 32) / 8, swz(row) = (row >> 2) & 3,
-//   KB = ceil(K / 32), Rpad = R rounded up to a multiple of 64 and of the
-//   GEMM tile extent along the rows.
+//   KB = ceil(K / 32) (or more: zero k-blocks), Rpad = R rounded up to a
+//   multiple of 64 and of the GEMM tile extent along the rows (plus
+//   ROW_SKEW_TILES tiles), plane_elems = KB * Rpad * 32 + PLANE_SKEW.
 //
 // So one k-block of a component is a row-major [Rpad][32] bf16 slab, 64 bytes
 // per row: a workgroup tile of T rows is one contiguous T*64-byte block that a
@@ -39,9 +40,24 @@ constexpr int KB_PER_PANEL = KPANEL / KBLK;
 
 __host__ __device__ inline int swz(int64_t row) { return (int)((row >> 2) & 3); }
 
+// Memory-channel staggering of the packed operands.  With power-of-two sizes
+// the k-block stride (Rpad x 64 B) and the plane stride are multiples of a
+// large power of two, and every copy of a tile's k-block (all planes) lands in
+// the same few L2 channels.  Two skews break that: Rpad gets ROW_SKEW_TILES
+// extra (zero) tiles, and consecutive planes are PLANE_SKEW elements further
+// apart than their KB x Rpad x 32 elements (a multiple of 512: planes stay
+// 1 KB aligned).
+constexpr int ROW_SKEW_TILES = 2;
+constexpr int64_t PLANE_SKEW = 2048;
+
+// Elements from one component plane to the next.
+__host__ __device__ inline int64_t plane_elems(int64_t KB, int64_t Rpad) {
+    return KB * Rpad * KBLK + PLANE_SKEW;
+}
+
 __host__ __device__ inline int64_t packed_index(int c, int64_t kb, int64_t row, int q, int64_t KB,
                                                 int64_t Rpad) {
-    return ((c * KB + kb) * Rpad + row) * KBLK + 8 * (q ^ swz(row));
+    return c * plane_elems(KB, Rpad) + (kb * Rpad + row) * KBLK + 8 * (q ^ swz(row));
 }
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }

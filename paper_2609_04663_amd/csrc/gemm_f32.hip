@@ -52,8 +52,8 @@ __global__ __launch_bounds__(256, 1) void gemm_f32_kernel(
 
     const char *Ag = reinterpret_cast<const char *>(Ap);
     const char *Bg = reinterpret_cast<const char *>(Bp);
-    const int64_t a_plane = (int64_t)KB * RpadA * 64;
-    const int64_t b_plane = (int64_t)KB * RpadB * 64;
+    const int64_t a_plane = plane_elems(KB, RpadA) * 2;
+    const int64_t b_plane = plane_elems(KB, RpadB) * 2;
 
     // Copy issue for one k-block: wave w moves 1 KB parts [RB w, RB w + RB) of
     // each A plane and [2w, 2w + 2) of each B plane, so every address is a

@@ -118,8 +118,8 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
 
     const char *Ag = reinterpret_cast<const char *>(Ap);
     const char *Bg = reinterpret_cast<const char *>(Bp);
-    const int64_t a_plane = (int64_t)KB * RpadA * 64;
-    const int64_t b_plane = (int64_t)KB * RpadB * 64;
+    const int64_t a_plane = plane_elems(KB, RpadA) * 2;
+    const int64_t b_plane = plane_elems(KB, RpadB) * 2;
 
     // Copy issue for one k-block: wave w moves 1 KB parts [w BM, (w + 1) BM) of
     // every A plane and part w of every B plane (wave-uniform base plus
@@ -417,8 +417,8 @@ __global__ __launch_bounds__(256, 1) void gemm_f64w_kernel(
 
     const char *Ag = reinterpret_cast<const char *>(Ap);
     const char *Bg = reinterpret_cast<const char *>(Bp);
-    const int64_t a_plane = (int64_t)KB * RpadA * 64;
-    const int64_t b_plane = (int64_t)KB * RpadB * 64;
+    const int64_t a_plane = plane_elems(KB, RpadA) * 2;
+    const int64_t b_plane = plane_elems(KB, RpadB) * 2;
 
     // Copy c of a k-block by wave w moves 1 KB part g = 4 c + w of the list
     // A parts (plane-major, 2 BMW parts a plane), then B parts: for BMW = 1,
@@ -743,7 +743,7 @@ __global__ __launch_bounds__(256, 1) void gemm_f64t_kernel(
     // the copied k-block's slab of plane 0 at the tile's first row / column.
     const char *Ag = reinterpret_cast<const char *>(Ap) + m0 * 64 + wave * 1024;
     const char *Bg = reinterpret_cast<const char *>(Bp) + n0 * 64 + wave * 1024;
-    const int64_t a_plane = (int64_t)KB * RpadA * 64, b_plane = (int64_t)KB * RpadB * 64;
+    const int64_t a_plane = plane_elems(KB, RpadA) * 2, b_plane = plane_elems(KB, RpadB) * 2;
     const int64_t a_kstep = RpadA * 64, b_kstep = RpadB * 64;
     auto issue = [&](const char *ak, const char *bk, char *dst, auto c_c) {
         constexpr int c = decltype(c_c)::value;
