@@ -118,6 +118,11 @@ def _configure(L):
     L.orc_ref_dd_entries.argtypes = [i64, i64, i64, p, i64, p, i64, i64, p, p, p, p]
     L.orc_absprod_entries.argtypes = [i64, p, i64, p, i64, i64, p, p, p]
     L.orc_num_threads.restype = ctypes.c_int
+    L.orc_set_num_threads.argtypes = [ctypes.c_int]
+    L.orc_sgemm_entries_from_comps.argtypes = [i64, i64, i64, p, p, i64, p, p, p, i64]
+    L.orc_dgemm_entries_from_slices.argtypes = [i64, i64, i64, p, p, i64, p, p, p, ctypes.c_int,
+                                                i64]
+    L.orc_dgemm_entries_from_slices.restype = u32
     L.orc_dot_bf16_f32.argtypes = [i64, p, p]
     L.orc_dot_bf16_f32.restype = ctypes.c_float
     return L
@@ -135,6 +140,37 @@ def _c(a, dtype):
 
 def num_threads() -> int:
     return lib().orc_num_threads()
+
+
+def set_num_threads(n: int):
+    """Threads of the oracle's OpenMP loops from now on."""
+    lib().orc_set_num_threads(int(n))
+
+
+def sgemm_entries_from_comps(Av, Bv, rows, cols, kc: int = KC):
+    """Entries (rows[e], cols[e]) of the emulated SGEMM from the components of
+    split_f32 (Av [3, M, K], Bv [3, K, N])."""
+    Av, Bv = _c(Av, np.uint16), _c(Bv, np.uint16)
+    _, M, K = Av.shape
+    N = Bv.shape[2]
+    r, c = _idx(rows, cols)
+    out = np.zeros(r.shape, dtype=np.float32)
+    lib().orc_sgemm_entries_from_comps(M, N, K, _ptr(Av), _ptr(Bv), r.size, _ptr(r), _ptr(c),
+                                       _ptr(out), int(kc))
+    return out
+
+
+def dgemm_entries_from_slices(Av, Bv, rows, cols, nprod: int, kc: int = KC):
+    """Entries of the emulated DGEMM from the slices of split_f64 (Av [6, M, K],
+    Bv [6, K, N]); returns (values, inexact-panel status)."""
+    Av, Bv = _c(Av, np.uint16), _c(Bv, np.uint16)
+    _, M, K = Av.shape
+    N = Bv.shape[2]
+    r, c = _idx(rows, cols)
+    out = np.zeros(r.shape, dtype=np.float64)
+    st = lib().orc_dgemm_entries_from_slices(M, N, K, _ptr(Av), _ptr(Bv), r.size, _ptr(r),
+                                             _ptr(c), _ptr(out), int(nprod), int(kc))
+    return out, int(st)
 
 
 def bf16_rne_f32(x: float) -> int:

@@ -116,6 +116,15 @@ static unsigned classify_bf16(uint16_t h, int source_nonzero) {
     return st;
 }
 
+/* Threads of the OpenMP loops below (the benchmark's one-core baseline). */
+void orc_set_num_threads(int n) {
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 int orc_num_threads(void) {
 #ifdef _OPENMP
     return omp_get_max_threads();
@@ -399,6 +408,15 @@ unsigned orc_emu_sgemm_entries(i64 M, i64 N, i64 K, const float *A, i64 lda, con
     return st;
 }
 
+/* Selected entries from components already split by orc_split_f32:
+   Av [3][M][K], Bv [3][K][N] (the benchmark times the split and the entries
+   apart). */
+void orc_sgemm_entries_from_comps(i64 M, i64 N, i64 K, const uint16_t *Av, const uint16_t *Bv,
+                                  i64 nent, const i64 *rows, const i64 *cols, float *out, i64 kc) {
+#pragma omp parallel for schedule(dynamic, 16)
+    for (i64 e = 0; e < nent; ++e) out[e] = sgemm_entry(K, kc, Av, Bv, M, N, rows[e], cols[e]);
+}
+
 /* ------------------------------------------------------------------------- */
 /* Emulated DGEMM, Algorithm fp64 / Eq. (fp64reconstruction). */
 
@@ -486,6 +504,23 @@ unsigned orc_emu_dgemm_entries(i64 M, i64 N, i64 K, const double *A, i64 lda, co
     free(Av);
     free(Bv);
     return st | st2;
+}
+
+/* Selected entries from slices already split by orc_split_f64: Av [6][M][K],
+   Bv [6][K][N]; returns the inexact-panel status (bit 16). */
+unsigned orc_dgemm_entries_from_slices(i64 M, i64 N, i64 K, const uint16_t *Av,
+                                       const uint16_t *Bv, i64 nent, const i64 *rows,
+                                       const i64 *cols, double *out, int nprod, i64 kc) {
+    int d = nprod_to_d(nprod);
+    if (d < 0) return 0xFFFFFFFFu;
+    unsigned st2 = 0;
+#pragma omp parallel for schedule(dynamic, 16) reduction(| : st2)
+    for (i64 e = 0; e < nent; ++e) {
+        unsigned s = 0;
+        out[e] = dgemm_entry(K, kc, d, Av, Bv, M, N, rows[e], cols[e], &s);
+        st2 |= s;
+    }
+    return st2;
 }
 
 /* ------------------------------------------------------------------------- */

@@ -384,3 +384,21 @@ def test_dgemm_inexact_flag_cases_are_not_vacuous():
     A = np.ldexp(S.make("uniform", 51, (2, 40), np.float64), -45)
     B = np.ldexp(S.make("uniform", 52, (40, 2), np.float64), -45)
     assert _inexact_by_definition(A, B, 21, 256) and not _inexact_by_definition(A, B, 6, 256)
+
+
+def test_entries_from_presplit_components_match():
+    """The benchmark's pre-split entry points give the bits of the plain ones."""
+    A = S.make("wide", 61, (9, 300), np.float64)
+    B = S.make("uniform", 62, (300, 7), np.float64)
+    rows = np.array([0, 3, 8, 8], np.int64)
+    cols = np.array([0, 6, 1, 6], np.int64)
+    sa, _, _, _ = O.split_f64(A)
+    sb, _, _, _ = O.split_f64(B)
+    for nprod in (6, 21, 36):
+        want, st = O.emu_dgemm_entries(A, B, rows, cols, nprod)
+        got, st2 = O.dgemm_entries_from_slices(sa, sb, rows, cols, nprod)
+        assert st == st2 == 0 and np.array_equal(got.view(np.uint64), want.view(np.uint64))
+    A32, B32 = A.astype(np.float32), B.astype(np.float32)
+    want, _ = O.emu_sgemm_entries(A32, B32, rows, cols)
+    got = O.sgemm_entries_from_comps(O.split_f32(A32)[0], O.split_f32(B32)[0], rows, cols)
+    assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
