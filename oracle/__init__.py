@@ -43,9 +43,26 @@ SPLIT_LITERAL = 1
 # into the FP64 result, C_mn = 2^(sA_m + sB_n) C'_mn.
 SCOPE_OPERAND = 0
 SCOPE_ROWCOL = 1
+# K-binned scope (an extension of the scale-aware split along the reduction):
+# the reduction indices k are grouped by the magnitude class of their product
+# terms, every group is computed as its own row/column-scaled emulated GEMM
+# (its own weights and exponent chains) and the groups are added in FP64,
+# group 0 (the largest terms) first.  The class of k is
+#   floor(-(ceil(log2 max_m |A~_mk|) + ceil(log2 max_n |B~_kn|)) / KBIN_WIDTH),
+# capped at KBIN_MAX - 1, with A~, B~ the row- and column-scaled operands of
+# the ROWCOL scope; a k whose column of A~ or row of B~ is zero contributes
+# exact zeros and is left out.
+SCOPE_KBIN = 2
+KBIN_WIDTH = 8
+KBIN_MAX = 8
+# Fallback (the "fallback handling" of Sec. 9 for inputs the split cannot
+# represent): when a DGEMM's status has any bit set, its product is the plain
+# FP64 GEMM of the inputs instead, and status bit ST_FALLBACK is added.
+FALLBACK_NONE = 0
+FALLBACK_FP64 = 1
 KC = 256  # reduction-panel length B_K of the paper's blocked loop (Sec. 6.1)
 
-ST_NAN, ST_RANGE, ST_SUBNORMAL, ST_OVERFLOW, ST_INEXACT32 = 1, 2, 4, 8, 16
+ST_NAN, ST_RANGE, ST_SUBNORMAL, ST_OVERFLOW, ST_INEXACT32, ST_FALLBACK = 1, 2, 4, 8, 16, 32
 # N_p(d) = |S_d| of Eq. (product-selection), six slices per operand, d = 1 .. 11
 NPROD_TO_D = {sum(1 for i in range(6) for j in range(6) if i + j < d): d for d in range(1, 12)}
 
@@ -258,8 +275,39 @@ def scaled_operands(A: np.ndarray, B: np.ndarray):
     return sA, sB, np.ldexp(A, -sA[:, None]), np.ldexp(B, -sB[None, :])
 
 
+def _ceil_log2_or_none(m: np.ndarray):
+    f, e = np.frexp(m)
+    return np.where(f == 0.5, e - 1, e)
+
+
+def kbin_classes(A: np.ndarray, B: np.ndarray) -> np.ndarray:
+    """Class of every reduction index k of the K-binned scope (-1: left out)."""
+    _, _, As, Bs = scaled_operands(A, B)
+    a = np.where(np.isfinite(As), np.abs(As), 0.0).max(axis=0) if As.shape[0] else np.zeros(As.shape[1])
+    b = np.where(np.isfinite(Bs), np.abs(Bs), 0.0).max(axis=1) if Bs.shape[1] else np.zeros(Bs.shape[0])
+    e = _ceil_log2_or_none(a) + _ceil_log2_or_none(b)
+    cls = np.minimum((-e) // KBIN_WIDTH, KBIN_MAX - 1)
+    return np.where((a > 0) & (b > 0), cls, -1).astype(np.int64)
+
+
 def emu_dgemm(A: np.ndarray, B: np.ndarray, nprod: int, mode: int = SPLIT_SYM, kc: int = KC,
               scope: int = SCOPE_OPERAND):
+    if scope == SCOPE_KBIN:
+        A, B = _c(A, np.float64), _c(B, np.float64)
+        cls = kbin_classes(A, B)
+        C = np.zeros((A.shape[0], B.shape[1]), dtype=np.float64)
+        st = 0
+        first = True
+        for b in range(KBIN_MAX):
+            ks = np.nonzero(cls == b)[0]
+            if ks.size == 0:
+                continue
+            Cb, sb = emu_dgemm(np.ascontiguousarray(A[:, ks]), np.ascontiguousarray(B[ks, :]),
+                               nprod, mode, kc, SCOPE_ROWCOL)
+            C = Cb if first else Cb + C            # FP64, group order
+            first = False
+            st |= sb
+        return C, st
     if scope == SCOPE_ROWCOL:
         sA, sB, As, Bs = scaled_operands(_c(A, np.float64), _c(B, np.float64))
         C, st = emu_dgemm(As, Bs, nprod, mode, kc)
@@ -276,6 +324,24 @@ def emu_dgemm(A: np.ndarray, B: np.ndarray, nprod: int, mode: int = SPLIT_SYM, k
 
 def emu_dgemm_entries(A, B, rows, cols, nprod: int, mode: int = SPLIT_SYM, kc: int = KC,
                       scope: int = SCOPE_OPERAND):
+    if scope == SCOPE_KBIN:
+        A, B = _c(A, np.float64), _c(B, np.float64)
+        cls = kbin_classes(A, B)
+        r, c = _idx(rows, cols)
+        out = np.zeros(r.shape, dtype=np.float64)
+        st = 0
+        first = True
+        for b in range(KBIN_MAX):
+            ks = np.nonzero(cls == b)[0]
+            if ks.size == 0:
+                continue
+            ob, sb = emu_dgemm_entries(np.ascontiguousarray(A[:, ks]),
+                                       np.ascontiguousarray(B[ks, :]), r, c, nprod, mode, kc,
+                                       SCOPE_ROWCOL)
+            out = ob if first else ob + out
+            first = False
+            st |= sb
+        return out, st
     if scope == SCOPE_ROWCOL:
         sA, sB, As, Bs = scaled_operands(_c(A, np.float64), _c(B, np.float64))
         r, c = _idx(rows, cols)
@@ -321,12 +387,16 @@ def emu_sgemm_ex(A, B, C=None, transa="N", transb="N", alpha=1.0, beta=0.0, kc: 
 
 
 def emu_dgemm_ex(A, B, nprod: int, C=None, transa="N", transb="N", alpha=1.0, beta=0.0,
-                 mode: int = SPLIT_SYM, kc: int = KC, scope: int = SCOPE_OPERAND):
+                 mode: int = SPLIT_SYM, kc: int = KC, scope: int = SCOPE_OPERAND,
+                 fallback: int = FALLBACK_NONE):
     opA, opB = _op(_c(A, np.float64), transa), _op(_c(B, np.float64), transb)
     M, N = opA.shape[0], opB.shape[1]
     if alpha == 0 or opA.shape[1] == 0:
         return _scale_only(C, beta, (M, N), np.float64), 0
     P, st = emu_dgemm(opA, opB, nprod, mode, kc, scope)
+    if fallback == FALLBACK_FP64 and st != 0:
+        P = ref_gemm_f64(opA, opB)                 # the plain FP64 GEMM of the inputs
+        st |= ST_FALLBACK
     return _blas_out(P, C, alpha, beta, np.float64), st
 
 
