@@ -68,6 +68,10 @@ extern "C" {
                                    FP32 and the result is not Eq.
                                    (fp64reconstruction) with exact panel products */
 
+#define EMU_STATUS_FALLBACK 32u /* (emu_dgemm with EMU_FALLBACK_FP64) the call's
+                                   split raised a bit above and C was computed by
+                                   the native FP64 fallback instead */
+
 /* FP64 split projection constant (Eq. fp64split).  SYM (default) uses
    Sigma = 0.75 * 2^(v+45): granularity 2^(v-8) for both signs, which is the
    reading that reproduces the paper's accuracy table.  LITERAL uses
@@ -155,6 +159,24 @@ int emu_sgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, floa
 int emu_dgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, double alpha,
                  const double *A, int64_t lda, const double *B, int64_t ldb, double beta,
                  double *C, int64_t ldc, int nprod);
+
+/* Fallback of the emulated DGEMM for inputs its split cannot represent (the
+   "fallback handling" of Sec. 9 and the "fallback extension" of Sec. 4.3),
+   for subsequent emu_dgemm, emu_dgemm_ex and emu_dgemm_noalloc calls.
+   EMU_FALLBACK_NONE (default): as in the paper, out-of-domain input is
+   computed anyway and only reported.  EMU_FALLBACK_FP64: when the split of
+   the call raises any EMU_STATUS_* bit (NaN or infinity, an entry outside
+   Eq. (bf16rangefp64) in the current scope, a subnormal, underflowed or
+   overflowed slice, a panel product that may be inexact in FP32), C is
+   recomputed as alpha op(A) op(B) + beta C by a plain FP64 GEMM (fused
+   multiply-adds, its own summation order) and EMU_STATUS_FALLBACK is reported
+   as well.  The decision is taken on the device: no host synchronisation; the
+   armed mode costs a kernel launch per call that does nothing unless the
+   fallback is needed, plus, for beta != 0, a copy of C in the workspace.
+   EMU_EINVAL for any other value. */
+#define EMU_FALLBACK_NONE 0
+#define EMU_FALLBACK_FP64 1
+int emu_set_fallback(int mode);
 
 /* Stream for subsequent calls (a hipStream_t); NULL selects the default
    stream.  Switching streams orders the new stream after the work already

@@ -46,6 +46,7 @@ hipStream_t g_stream = nullptr;
 hipEvent_t g_switch_event = nullptr;   // orders a new stream after the previous one
 int g_split_mode = EMU_SPLIT_SYM;
 int g_split_scope = EMU_SCOPE_OPERAND;
+int g_fallback = EMU_FALLBACK_NONE;
 std::string g_err;
 
 // Workspace: [status word (offset 0), the FP64 split state slots of two
@@ -280,6 +281,13 @@ int emu_set_split_mode(int mode) {
     return EMU_OK;
 }
 
+int emu_set_fallback(int mode) {
+    if (mode != EMU_FALLBACK_NONE && mode != EMU_FALLBACK_FP64)
+        return fail(EMU_EINVAL, "fallback must be EMU_FALLBACK_NONE or EMU_FALLBACK_FP64");
+    g_fallback = mode;
+    return EMU_OK;
+}
+
 int emu_set_split_scope(int scope) {
     if (scope != EMU_SCOPE_OPERAND && scope != EMU_SCOPE_ROWCOL)
         return fail(EMU_EINVAL, "split scope must be EMU_SCOPE_OPERAND or EMU_SCOPE_ROWCOL");
@@ -417,34 +425,69 @@ int emu_sgemm(int64_t M, int64_t N, int64_t K, const float *A, int64_t lda, cons
 namespace {
 
 // Bytes of workspace (after the header) an emulated DGEMM of depth d needs.
-size_t dgemm_ws_bytes(int64_t M, int64_t N, int64_t K, int d, bool scaled, Shape *sp) {
+// How one emulated DGEMM runs: with the row/column weights of the scale-aware
+// split, and with the native FP64 fallback armed.
+struct DgemmOpts {
+    bool scaled;
+    bool fallback;
+};
+
+DgemmOpts current_opts() {
+    return {g_split_scope != EMU_SCOPE_OPERAND, g_fallback == EMU_FALLBACK_FP64};
+}
+
+// Workspace areas of one emulated DGEMM after the header: packed planes, then
+// (256-byte aligned) the weights of the scale-aware split, then a copy of C
+// for a fallback that must still read beta C.
+struct DgemmLayout {
+    Shape s;
+    size_t scale_off, csave_off, bytes;
+};
+
+DgemmLayout dgemm_layout(int64_t M, int64_t N, int64_t K, int d, DgemmOpts o, double beta) {
+    DgemmLayout L;
     // the DGEMM kernel's tile rows and k-block multiple (padding is zero)
     const int64_t KB = (K + KBLK - 1) / KBLK;
-    const Shape s = plan(M, N, K, dgemm_planes(d), dgemm_tile_rows(d, M, N, KB), DGEMM_NT,
-                         dgemm_kb_padded(d, M, N, KB));
-    if (sp) *sp = s;
-    return s.bytesA + s.bytesB + (scaled ? scale_bytes(M, N) : 0);
+    L.s = plan(M, N, K, dgemm_planes(d), dgemm_tile_rows(d, M, N, KB), DGEMM_NT,
+               dgemm_kb_padded(d, M, N, KB));
+    auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+    L.scale_off = up(L.s.bytesA + L.s.bytesB);
+    L.csave_off = up(L.scale_off + (o.scaled ? scale_bytes(M, N) : 0));
+    L.bytes = L.csave_off + ((o.fallback && beta != 0.0) ? (size_t)M * N * sizeof(double) : 0);
+    return L;
 }
+
+// The accumulated status word (offset 0 of a workspace header) and the word of
+// the current call (offset 64) that an armed fallback reads.
+unsigned *ws_call_status(char *base) { return reinterpret_cast<unsigned *>(base + 64); }
 
 // The emulated DGEMM on a workspace at base (header, planes, weights), after
 // argument validation; M, N, K > 0 and alpha != 0.
-int dgemm_run(char *base, bool ta, bool tb, int64_t M, int64_t N, int64_t K, double alpha,
-              const double *A, int64_t lda, const double *B, int64_t ldb, double beta, double *C,
-              int64_t ldc, int d) {
+int dgemm_run(char *base, DgemmOpts o, bool ta, bool tb, int64_t M, int64_t N, int64_t K,
+              double alpha, const double *A, int64_t lda, const double *B, int64_t ldb,
+              double beta, double *C, int64_t ldc, int d) {
     // Only the slices the retained products read are materialised; the levels
     // after them never influence the earlier slices.
     const int np = dgemm_planes(d);
-    const bool scaled = g_split_scope == EMU_SCOPE_ROWCOL;
-    Shape s;
-    (void)dgemm_ws_bytes(M, N, K, d, scaled, &s);
+    const DgemmLayout L = dgemm_layout(M, N, K, d, o, beta);
+    const Shape &s = L.s;
     uint16_t *Ap = ws_planes(base, 0), *Bp = ws_planes(base, s.bytesA);
     F64SplitState *st = ws_states(base);
-    const ScaleArea sc = ws_scales(base, s.bytesA + s.bytesB, M, N);
+    const ScaleArea sc = ws_scales(base, L.scale_off, M, N);
+    double *Csave = reinterpret_cast<double *>(base + HDR + L.csave_off);
     // stored shapes: A is M x K ('N') or K x M ('T'); B is K x N ('N') or N x K ('T')
     const int64_t ar = ta ? K : M, ac = ta ? M : K, br = tb ? N : K, bc = tb ? K : N;
     prof_mark(0);
     hipError_t e = hipSuccess;
-    if (scaled) {
+    // an armed fallback reads the flags of this call alone: they go to the
+    // call's own word (cleared by a kernel, not a memset), and the fallback
+    // kernel adds them to the accumulated word
+    unsigned *split_status = o.fallback ? ws_call_status(base) : ws_status(base);
+    if (o.fallback) {
+        e = launch_fill_f32(reinterpret_cast<float *>(split_status), 1, 1, 1, g_stream);
+        if (e != hipSuccess) return hip_fail(e, "clear call status");
+    }
+    if (o.scaled) {
         // weights: rows of op(A), columns of op(B) (the scale-aware split)
         e = launch_scale_exponents(A, ar, ac, lda, ta, sc.mb, sc.sa, g_stream);
         if (e != hipSuccess) return hip_fail(e, "scale_exponents(A)");
@@ -454,14 +497,24 @@ int dgemm_run(char *base, bool ta, bool tb, int64_t M, int64_t N, int64_t K, dou
     // both operands in one launch per phase: op(A)'s rows are A's rows ('N') or
     // A's columns ('T', packed as a B operand), op(B)'s columns likewise
     const F64SplitOperand ops[2] = {
-        {A, ar, ac, lda, ta ? 1 : 0, scaled ? sc.sa : nullptr, Ap, s.RpadA, st},
-        {B, br, bc, ldb, tb ? 0 : 1, scaled ? sc.sb : nullptr, Bp, s.RpadB, st + F64_SLOTS}};
-    e = launch_split_f64(ops, 2, s.KB, np, g_split_mode, d, ws_status(base), g_stream);
+        {A, ar, ac, lda, ta ? 1 : 0, o.scaled ? sc.sa : nullptr, Ap, s.RpadA, st},
+        {B, br, bc, ldb, tb ? 0 : 1, o.scaled ? sc.sb : nullptr, Bp, s.RpadB, st + F64_SLOTS}};
+    e = launch_split_f64(ops, 2, s.KB, np, g_split_mode, d, split_status, g_stream);
     if (e != hipSuccess) return hip_fail(e, "split_f64");
     prof_mark(1);
-    e = launch_gemm_f64(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, scaled ? sc.sa : nullptr,
-                        scaled ? sc.sb : nullptr, alpha, beta, d, g_stream);
+    const bool save_c = o.fallback && beta != 0.0;
+    if (save_c) {
+        e = launch_copy_matrix_f64(C, ldc, Csave, N, M, N, g_stream);
+        if (e != hipSuccess) return hip_fail(e, "save C");
+    }
+    e = launch_gemm_f64(Ap, Bp, C, M, N, s.KB, s.RpadA, s.RpadB, ldc, o.scaled ? sc.sa : nullptr,
+                        o.scaled ? sc.sb : nullptr, alpha, beta, d, g_stream);
     if (e != hipSuccess) return hip_fail(e, "gemm_f64");
+    if (o.fallback) {
+        e = launch_fallback_dgemm(split_status, ws_status(base), M, N, K, alpha, A, lda, ta, B, ldb,
+                                  tb, beta, save_c ? Csave : C, save_c ? N : ldc, C, ldc, g_stream);
+        if (e != hipSuccess) return hip_fail(e, "fallback_dgemm");
+    }
     prof_mark(2);
     return EMU_OK;
 }
@@ -502,9 +555,10 @@ int emu_dgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, doub
     if (!dgemm_prologue(transa, transb, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, nprod, &d,
                         &ta, &tb, &rc))
         return rc;
-    rc = ensure_workspace(dgemm_ws_bytes(M, N, K, d, g_split_scope == EMU_SCOPE_ROWCOL, nullptr));
+    const DgemmOpts o = current_opts();
+    rc = ensure_workspace(dgemm_layout(M, N, K, d, o, beta).bytes);
     if (rc) return rc;
-    return dgemm_run(g_ws.base, ta, tb, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, d);
+    return dgemm_run(g_ws.base, o, ta, tb, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, d);
 }
 
 int emu_dgemm_noalloc(int64_t M, int64_t N, int64_t K, const double *A, int64_t lda,
@@ -514,8 +568,8 @@ int emu_dgemm_noalloc(int64_t M, int64_t N, int64_t K, const double *A, int64_t 
     if (!dgemm_prologue('N', 'N', M, N, K, 1.0, A, lda, B, ldb, 0.0, C, ldc, nprod, &d, &ta, &tb,
                         &rc))
         return rc;
-    const size_t need =
-        HDR + dgemm_ws_bytes(M, N, K, d, g_split_scope == EMU_SCOPE_ROWCOL, nullptr);
+    const DgemmOpts o = current_opts();
+    const size_t need = HDR + dgemm_layout(M, N, K, d, o, 0.0).bytes;
     if (need > NOALLOC_BYTES) {
         g_err = "emu_dgemm_noalloc: this problem needs " + std::to_string(need) +
                 " bytes of scratch, more than the fixed " + std::to_string(NOALLOC_BYTES);
@@ -523,7 +577,7 @@ int emu_dgemm_noalloc(int64_t M, int64_t N, int64_t K, const double *A, int64_t 
     }
     char *base = scratch_for_current_device(&rc);
     if (!base) return rc;
-    return dgemm_run(base, false, false, M, N, K, 1.0, A, lda, B, ldb, 0.0, C, ldc, d);
+    return dgemm_run(base, o, false, false, M, N, K, 1.0, A, lda, B, ldb, 0.0, C, ldc, d);
 }
 
 int emu_dgemm(int64_t M, int64_t N, int64_t K, const double *A, int64_t lda, const double *B,

@@ -63,7 +63,8 @@ __host__ __device__ inline int64_t packed_index(int c, int64_t kb, int64_t row, 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
 // Status bits (same values as EMU_STATUS_* in emu.h).
-constexpr unsigned ST_NAN = 1u, ST_RANGE = 2u, ST_SUBNORMAL = 4u, ST_OVERFLOW = 8u, ST_INEXACT = 16u;
+constexpr unsigned ST_NAN = 1u, ST_RANGE = 2u, ST_SUBNORMAL = 4u, ST_OVERFLOW = 8u, ST_INEXACT = 16u,
+                   ST_FALLBACK = 32u;
 
 // Device state of the FP64 split of one operand: the operand-wide per-level
 // maxima (bit patterns of non-negative doubles, whose unsigned order is the
@@ -130,6 +131,15 @@ hipError_t launch_scale_exponents(const double *X, int64_t rows, int64_t cols, i
 hipError_t launch_unpack(const uint16_t *P, int nc, int64_t KB, int64_t Rpad, int64_t rows,
                          int64_t cols, bool as_b, uint16_t *out, hipStream_t s);
 hipError_t launch_copy_v(const F64SplitState *st, int32_t *v, hipStream_t s);
+// Native FP64 fallback: C = alpha op(A) op(B) + beta Cin when *call_status is
+// nonzero (then also status |= *call_status | ST_FALLBACK); nothing otherwise.
+hipError_t launch_fallback_dgemm(const unsigned *call_status, unsigned *status, int64_t M,
+                                 int64_t N, int64_t K, double alpha, const double *A, int64_t lda,
+                                 bool ta, const double *B, int64_t ldb, bool tb, double beta,
+                                 const double *Cin, int64_t ldcin, double *C, int64_t ldc,
+                                 hipStream_t s);
+hipError_t launch_copy_matrix_f64(const double *src, int64_t lds, double *dst, int64_t ldd,
+                                  int64_t M, int64_t N, hipStream_t s);
 // alpha, beta: C = alpha P + beta C (see out_update); 1, 0 stores P
 // Split-K factor of the emulated SGEMM: 1 unless the output tiles fill at most
 // half of the chip, else up to 16 splits of whole reduction panels.  splits > 1 needs part:
