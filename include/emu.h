@@ -93,6 +93,22 @@ extern "C" {
    largest magnitude, and results that neither overflow nor underflow FP64. */
 #define EMU_SCOPE_OPERAND 0
 #define EMU_SCOPE_ROWCOL 1
+/* KBIN: the scale-aware form extended along the reduction, for products whose
+   terms differ in magnitude along k (for example some rows of B far larger
+   than the others), which row and column weights cannot normalise.  With the
+   ROWCOL weights sA, sB, the class of reduction index k is
+     min(7, floor(-(ceil(log2 max_m |A_mk 2^-sA_m|) + ceil(log2 max_n |B_kn 2^-sB_n|)) / 8))
+   (op(A), op(B); an index whose column of op(A) or row of op(B) is zero adds
+   exact zeros and is left out).  The indices of each class form a group; each
+   group is an emulated DGEMM of its columns of op(A) and rows of op(B) in the
+   ROWCOL scope (its own weights and exponent chains), and the groups are added
+   in FP64 in ascending class order, S = P_0, then S = fl(P_c + S); the
+   call returns fl(fl(alpha S) + fl(beta C)).  The call synchronises its stream
+   once (to size the groups) and uses workspace for the gathered groups
+   (8 (M + N) K bytes) and, unless alpha = 1 and beta = 0, for S (8 M N).
+   Not available to emu_dgemm_noalloc (EMU_EINVAL).  emu_split_f64 and the
+   status checks behave as in ROWCOL. */
+#define EMU_SCOPE_KBIN 2
 
 /* Emulated SGEMM, Algorithm fp32 (Sec. 4.2, Eq. fp32split and fp32six):
    each FP32 operand is split into three BF16 components; the six products
@@ -191,7 +207,7 @@ int emu_set_stream(void *hip_stream);
 int emu_set_split_mode(int mode);
 
 /* Exponent scope of the FP64 split for subsequent emu_dgemm and emu_split_f64
-   calls: EMU_SCOPE_OPERAND (default) or EMU_SCOPE_ROWCOL (see above).  In the
+   calls: EMU_SCOPE_OPERAND (default), EMU_SCOPE_ROWCOL or EMU_SCOPE_KBIN (see above).  In the
    ROWCOL scope the domain checks behind EMU_STATUS_RANGE apply to the scaled
    operands.  EMU_EINVAL for any other value. */
 int emu_set_split_scope(int scope);

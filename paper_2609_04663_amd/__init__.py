@@ -31,7 +31,7 @@ STATUS_NAN, STATUS_RANGE, STATUS_SUBNORMAL, STATUS_OVERFLOW, STATUS_INEXACT = 1,
 STATUS_FALLBACK = 32
 FALLBACK_NONE, FALLBACK_FP64 = 0, 1
 SPLIT_SYM, SPLIT_LITERAL = 0, 1
-SCOPE_OPERAND, SCOPE_ROWCOL = 0, 1
+SCOPE_OPERAND, SCOPE_ROWCOL, SCOPE_KBIN = 0, 1, 2
 # the paper's product counts N_p(d), d = 3 .. 6 (Eq. fp64productcounts) ...
 NPROD = (6, 10, 15, 21)
 # ... and every depth d = 1 .. 11 of the selection S_d (Eq. product-selection)

@@ -17,7 +17,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libemu.so")
-SOURCES = ["split.hip", "gemm_f32.hip", "gemm_f64.hip", "fallback.hip", "emu_api.hip"]
+SOURCES = ["split.hip", "gemm_f32.hip", "gemm_f64.hip", "fallback.hip", "kbin.hip", "emu_api.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -289,8 +289,9 @@ int emu_set_fallback(int mode) {
 }
 
 int emu_set_split_scope(int scope) {
-    if (scope != EMU_SCOPE_OPERAND && scope != EMU_SCOPE_ROWCOL)
-        return fail(EMU_EINVAL, "split scope must be EMU_SCOPE_OPERAND or EMU_SCOPE_ROWCOL");
+    if (scope != EMU_SCOPE_OPERAND && scope != EMU_SCOPE_ROWCOL && scope != EMU_SCOPE_KBIN)
+        return fail(EMU_EINVAL,
+                    "split scope must be EMU_SCOPE_OPERAND, EMU_SCOPE_ROWCOL or EMU_SCOPE_KBIN");
     g_split_scope = scope;
     return EMU_OK;
 }
@@ -462,10 +463,12 @@ DgemmLayout dgemm_layout(int64_t M, int64_t N, int64_t K, int d, DgemmOpts o, do
 unsigned *ws_call_status(char *base) { return reinterpret_cast<unsigned *>(base + 64); }
 
 // The emulated DGEMM on a workspace at base (header, planes, weights), after
-// argument validation; M, N, K > 0 and alpha != 0.
+// argument validation; M, N, K > 0 and alpha != 0.  status_to: the word the
+// split's flags go to when the fallback is not armed (null: the accumulated
+// word).
 int dgemm_run(char *base, DgemmOpts o, bool ta, bool tb, int64_t M, int64_t N, int64_t K,
               double alpha, const double *A, int64_t lda, const double *B, int64_t ldb,
-              double beta, double *C, int64_t ldc, int d) {
+              double beta, double *C, int64_t ldc, int d, unsigned *status_to = nullptr) {
     // Only the slices the retained products read are materialised; the levels
     // after them never influence the earlier slices.
     const int np = dgemm_planes(d);
@@ -482,7 +485,8 @@ int dgemm_run(char *base, DgemmOpts o, bool ta, bool tb, int64_t M, int64_t N, i
     // an armed fallback reads the flags of this call alone: they go to the
     // call's own word (cleared by a kernel, not a memset), and the fallback
     // kernel adds them to the accumulated word
-    unsigned *split_status = o.fallback ? ws_call_status(base) : ws_status(base);
+    unsigned *split_status =
+        o.fallback ? ws_call_status(base) : (status_to ? status_to : ws_status(base));
     if (o.fallback) {
         e = launch_fill_f32(reinterpret_cast<float *>(split_status), 1, 1, 1, g_stream);
         if (e != hipSuccess) return hip_fail(e, "clear call status");
@@ -516,6 +520,103 @@ int dgemm_run(char *base, DgemmOpts o, bool ta, bool tb, int64_t M, int64_t N, i
         if (e != hipSuccess) return hip_fail(e, "fallback_dgemm");
     }
     prof_mark(2);
+    return EMU_OK;
+}
+
+std::vector<int> g_kbin_idx;   // host copy of the K-binned index lists
+
+// The K-binned scope: classes of the reduction indices on the device, one
+// stream synchronisation to read them, then for every class in ascending
+// order the gather of its columns of op(A) and rows of op(B) and a row/column
+// scaled emulated DGEMM of the group, added in FP64 to the previous groups'
+// sum (the first group stores, the others use the beta = 1 update, which adds
+// fl(P_g + S)); the BLAS update alpha S + beta C follows unless alpha = 1 and
+// beta = 0 (then the groups accumulate in C itself).  An armed fallback reads
+// the flags of all groups and replaces the whole result.
+int dgemm_kbin(bool ta, bool tb, int64_t M, int64_t N, int64_t K, double alpha, const double *A,
+               int64_t lda, const double *B, int64_t ldb, double beta, double *C, int64_t ldc,
+               int d) {
+    const bool fb = g_fallback == EMU_FALLBACK_FP64;
+    const bool direct = alpha == 1.0 && beta == 0.0;
+    auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+    // workspace after the area of the largest group's DGEMM (its planes and weights)
+    size_t off = up(dgemm_layout(M, N, K, d, {true, false}, 0.0).bytes);
+    const int64_t MN = M > N ? M : N;
+    const size_t o_sa = off;  off = up(off + (size_t)M * 4);
+    const size_t o_sb = off;  off = up(off + (size_t)N * 4);
+    const size_t o_mx = off;  off = up(off + (size_t)MN * 8);
+    const size_t o_ma = off;  off = up(off + (size_t)K * 8);
+    const size_t o_mb = off;  off = up(off + (size_t)K * 8);
+    const size_t o_cl = off;  off = up(off + (size_t)K * 4);
+    const size_t o_ix = off;  off = up(off + (size_t)K * 4);
+    const size_t o_ga = off;  off = up(off + (size_t)M * K * 8);
+    const size_t o_gb = off;  off = up(off + (size_t)K * N * 8);
+    const size_t o_p = off;   off = up(off + (direct ? 0 : (size_t)M * N * 8));
+    int rc = ensure_workspace(off);
+    if (rc) return rc;
+    char *base = g_ws.base, *w = g_ws.base + HDR;
+    int *sa = reinterpret_cast<int *>(w + o_sa), *sb = reinterpret_cast<int *>(w + o_sb);
+    auto *mx = reinterpret_cast<unsigned long long *>(w + o_mx);
+    auto *ma = reinterpret_cast<unsigned long long *>(w + o_ma);
+    auto *mb = reinterpret_cast<unsigned long long *>(w + o_mb);
+    int *cls = reinterpret_cast<int *>(w + o_cl), *idx = reinterpret_cast<int *>(w + o_ix);
+    double *GA = reinterpret_cast<double *>(w + o_ga), *GB = reinterpret_cast<double *>(w + o_gb);
+    double *P = reinterpret_cast<double *>(w + o_p);
+    unsigned *acc_st = ws_status(base), *call_st = ws_call_status(base);
+    const int64_t ar = ta ? K : M, ac = ta ? M : K, br = tb ? N : K, bc = tb ? K : N;
+    hipError_t e = hipSuccess;
+    if (fb) {
+        e = launch_fill_f32(reinterpret_cast<float *>(call_st), 1, 1, 1, g_stream);
+        if (e != hipSuccess) return hip_fail(e, "clear call status");
+    }
+    e = launch_scale_exponents(A, ar, ac, lda, ta, mx, sa, g_stream);
+    if (e == hipSuccess) e = launch_scale_exponents(B, br, bc, ldb, !tb, mx, sb, g_stream);
+    if (e == hipSuccess)
+        e = launch_kbin_classes(A, lda, ta, B, ldb, tb, M, N, K, sa, sb, ma, mb, KBIN_WIDTH,
+                                KBIN_MAX, cls, g_stream);
+    if (e != hipSuccess) return hip_fail(e, "kbin classes");
+    std::vector<int> h((size_t)K);
+    e = hipMemcpyAsync(h.data(), cls, (size_t)K * 4, hipMemcpyDeviceToHost, g_stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(g_stream);
+    if (e != hipSuccess) return hip_fail(e, "kbin classes to the host");
+    // the index lists stay alive in g_kbin_idx until the next call, which
+    // synchronises the stream before it rewrites them
+    std::vector<int> &ks = g_kbin_idx;
+    ks.clear();
+    std::vector<std::pair<size_t, int64_t>> groups;   // (first index in ks, size)
+    for (int c = 0; c < KBIN_MAX; ++c) {
+        const size_t first = ks.size();
+        for (int64_t k = 0; k < K; ++k)
+            if (h[(size_t)k] == c) ks.push_back((int)k);
+        if (ks.size() > first) groups.emplace_back(first, (int64_t)(ks.size() - first));
+    }
+    if (groups.empty()) {   // every product term is an exact zero
+        e = launch_scale_c_f64(C, M, N, ldc, beta, g_stream);
+        return e == hipSuccess ? EMU_OK : hip_fail(e, "scale C");
+    }
+    e = hipMemcpyAsync(idx, ks.data(), ks.size() * 4, hipMemcpyHostToDevice, g_stream);
+    if (e != hipSuccess) return hip_fail(e, "kbin index upload");
+    double *T = direct ? C : P;
+    const int64_t ldt = direct ? ldc : N;
+    for (size_t g = 0; g < groups.size(); ++g) {
+        const int64_t kb = groups[g].second;
+        e = launch_kbin_gather(A, lda, ta, B, ldb, tb, M, N, idx + groups[g].first, kb, GA, GB,
+                               g_stream);
+        if (e != hipSuccess) return hip_fail(e, "kbin gather");
+        rc = dgemm_run(base, {true, false}, false, false, M, N, kb, 1.0, GA, kb, GB, N,
+                       g == 0 ? 0.0 : 1.0, T, ldt, d, fb ? call_st : acc_st);
+        if (rc) return rc;
+    }
+    if (fb) {
+        // C is untouched unless direct (then beta = 0 and C is not read)
+        e = launch_fallback_dgemm(call_st, acc_st, M, N, K, alpha, A, lda, ta, B, ldb, tb, beta,
+                                  C, ldc, C, ldc, g_stream);
+        if (e != hipSuccess) return hip_fail(e, "fallback_dgemm");
+    }
+    if (!direct) {
+        e = launch_axpby_f64(P, N, C, ldc, M, N, alpha, beta, fb ? call_st : nullptr, g_stream);
+        if (e != hipSuccess) return hip_fail(e, "alpha P + beta C");
+    }
     return EMU_OK;
 }
 
@@ -555,6 +656,8 @@ int emu_dgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, doub
     if (!dgemm_prologue(transa, transb, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, nprod, &d,
                         &ta, &tb, &rc))
         return rc;
+    if (g_split_scope == EMU_SCOPE_KBIN)
+        return dgemm_kbin(ta, tb, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, d);
     const DgemmOpts o = current_opts();
     rc = ensure_workspace(dgemm_layout(M, N, K, d, o, beta).bytes);
     if (rc) return rc;
@@ -568,6 +671,8 @@ int emu_dgemm_noalloc(int64_t M, int64_t N, int64_t K, const double *A, int64_t 
     if (!dgemm_prologue('N', 'N', M, N, K, 1.0, A, lda, B, ldb, 0.0, C, ldc, nprod, &d, &ta, &tb,
                         &rc))
         return rc;
+    if (g_split_scope == EMU_SCOPE_KBIN)
+        return fail(EMU_EINVAL, "emu_dgemm_noalloc: the K-binned scope needs the growing workspace");
     const DgemmOpts o = current_opts();
     const size_t need = HDR + dgemm_layout(M, N, K, d, o, 0.0).bytes;
     if (need > NOALLOC_BYTES) {
@@ -620,7 +725,7 @@ int emu_split_f64(int64_t R, int64_t Cc, const double *X, int64_t ldx, int as_b,
     g_err.clear();
     const int64_t rows = as_b ? Cc : R, K = as_b ? R : Cc;
     const Shape s = plan(rows, 1, K, 6, ROW_GROUP, ROW_GROUP);
-    const bool scaled = g_split_scope == EMU_SCOPE_ROWCOL;
+    const bool scaled = g_split_scope != EMU_SCOPE_OPERAND;   // KBIN splits as ROWCOL here
     rc = ensure_workspace((s.bytesA > 0 ? s.bytesA : 1) + (scaled ? scale_bytes(rows, 0) : 0));
     if (rc) return rc;
     uint16_t *P = ws_planes(0);

@@ -140,6 +140,21 @@ hipError_t launch_fallback_dgemm(const unsigned *call_status, unsigned *status, 
                                  hipStream_t s);
 hipError_t launch_copy_matrix_f64(const double *src, int64_t lds, double *dst, int64_t ldd,
                                   int64_t M, int64_t N, hipStream_t s);
+// K-binned scope: the class of every reduction index of op(A) op(B) (-1: left
+// out) from the ROWCOL weights sa, sb; ma, mb: K 64-bit words of scratch each.
+constexpr int KBIN_WIDTH = 8, KBIN_MAX = 8;
+hipError_t launch_kbin_classes(const double *A, int64_t lda, bool ta, const double *B, int64_t ldb,
+                               bool tb, int64_t M, int64_t N, int64_t K, const int *sa,
+                               const int *sb, unsigned long long *ma, unsigned long long *mb,
+                               int width, int ncls, int *cls, hipStream_t s);
+// op(A)'s columns and op(B)'s rows idx[0 .. kb) into row-major M x kb and kb x N
+hipError_t launch_kbin_gather(const double *A, int64_t lda, bool ta, const double *B, int64_t ldb,
+                              bool tb, int64_t M, int64_t N, const int *idx, int64_t kb,
+                              double *GA, double *GB, hipStream_t s);
+// C = alpha P + beta C (the BLAS update), skipped when *skip_if is nonzero
+hipError_t launch_axpby_f64(const double *P, int64_t ldp, double *C, int64_t ldc, int64_t M,
+                            int64_t N, double alpha, double beta, const unsigned *skip_if,
+                            hipStream_t s);
 // alpha, beta: C = alpha P + beta C (see out_update); 1, 0 stores P
 // Split-K factor of the emulated SGEMM: 1 unless the output tiles fill at most
 // half of the chip, else up to 16 splits of whole reduction panels.  splits > 1 needs part:

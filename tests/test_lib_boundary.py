@@ -102,8 +102,9 @@ def test_split_mode_and_status_arguments(L):
 
 def test_split_scope_and_scale_hook_arguments(L):
     import paper_2609_04663_amd as emu
-    assert L.emu_set_split_scope(2) == emu.EMU_EINVAL
+    assert L.emu_set_split_scope(3) == emu.EMU_EINVAL
     assert L.emu_set_split_scope(-1) == emu.EMU_EINVAL
+    assert L.emu_set_split_scope(emu.SCOPE_KBIN) == emu.EMU_OK
     assert L.emu_set_split_scope(emu.SCOPE_ROWCOL) == emu.EMU_OK
     assert L.emu_set_split_scope(emu.SCOPE_OPERAND) == emu.EMU_OK
     assert L.emu_scale_exponents(-1, 4, P, 4, 0, P) == emu.EMU_EINVAL      # negative R
