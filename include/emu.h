@@ -194,6 +194,20 @@ int emu_dgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, doub
 #define EMU_FALLBACK_FP64 1
 int emu_set_fallback(int mode);
 
+/* How subsequent emu_sgemm and emu_sgemm_ex calls split their operands
+   (Eq. fp32split; Sec. 6.2 weighs the two ways):
+   EMU_SGEMM_SPLIT_PASS (default): a split kernel writes the three BF16 planes
+   of both operands to the workspace, and the product kernel reads them;
+   EMU_SGEMM_SPLIT_STREAMED: the product kernel reads op(A) and op(B) in FP32
+   and splits every k-block itself, in each workgroup that uses it, with the
+   split kernel's arithmetic (128 x 128 output tiles): no planes in HBM,
+   workspace only for split-reduction partial sums, the same status bits, and
+   the same result bits whenever both ways cut the reduction into the same
+   number of parts.  EMU_EINVAL for any other value. */
+#define EMU_SGEMM_SPLIT_PASS 0
+#define EMU_SGEMM_SPLIT_STREAMED 1
+int emu_set_sgemm_split(int mode);
+
 /* Stream for subsequent calls (a hipStream_t); NULL selects the default
    stream.  Switching streams orders the new stream after the work already
    queued on the previous one (an event dependency, no host synchronisation),

@@ -30,6 +30,7 @@ EMU_OK, EMU_EINVAL, EMU_EHIP, EMU_ENOMEM = 0, 1, 2, 3
 STATUS_NAN, STATUS_RANGE, STATUS_SUBNORMAL, STATUS_OVERFLOW, STATUS_INEXACT = 1, 2, 4, 8, 16
 STATUS_FALLBACK = 32
 FALLBACK_NONE, FALLBACK_FP64 = 0, 1
+SGEMM_SPLIT_PASS, SGEMM_SPLIT_STREAMED = 0, 1
 SPLIT_SYM, SPLIT_LITERAL = 0, 1
 SCOPE_OPERAND, SCOPE_ROWCOL, SCOPE_KBIN = 0, 1, 2
 # the paper's product counts N_p(d), d = 3 .. 6 (Eq. fp64productcounts) ...
@@ -41,7 +42,7 @@ EXPORTS = ("emu_sgemm", "emu_dgemm", "emu_set_stream", "emu_set_split_mode",
            "emu_domain_status", "emu_last_error", "emu_release_workspace",
            "emu_workspace_bytes", "emu_split_f32", "emu_split_f64", "emu_profile_enable",
            "emu_profile_read", "emu_set_split_scope", "emu_scale_exponents", "emu_sgemm_ex",
-           "emu_dgemm_ex", "emu_dgemm_noalloc", "emu_set_fallback")
+           "emu_dgemm_ex", "emu_dgemm_noalloc", "emu_set_fallback", "emu_set_sgemm_split")
 
 
 class EmuError(RuntimeError):
@@ -69,6 +70,7 @@ def lib() -> ctypes.CDLL:
         L.emu_set_split_mode.argtypes = [ci]
         L.emu_set_split_scope.argtypes = [ci]
         L.emu_set_fallback.argtypes = [ci]
+        L.emu_set_sgemm_split.argtypes = [ci]
         ch, f32, f64 = ctypes.c_char, ctypes.c_float, ctypes.c_double
         L.emu_sgemm_ex.argtypes = [ch, ch, i64, i64, i64, f32, p, i64, p, i64, f32, p, i64]
         L.emu_dgemm_ex.argtypes = [ch, ch, i64, i64, i64, f64, p, i64, p, i64, f64, p, i64, ci]
@@ -84,7 +86,8 @@ def lib() -> ctypes.CDLL:
                      "emu_domain_status", "emu_release_workspace", "emu_split_f32",
                      "emu_split_f64", "emu_profile_enable", "emu_profile_read",
                      "emu_set_split_scope", "emu_scale_exponents", "emu_sgemm_ex",
-                     "emu_dgemm_ex", "emu_dgemm_noalloc", "emu_set_fallback"):
+                     "emu_dgemm_ex", "emu_dgemm_noalloc", "emu_set_fallback",
+                     "emu_set_sgemm_split"):
             getattr(L, name).restype = ci
         _lib = L
     return _lib
@@ -249,6 +252,12 @@ def split_f64(X: torch.Tensor, as_b: bool = False):
 
 def set_split_mode(mode: int):
     _check(lib().emu_set_split_mode(int(mode)))
+
+
+def set_sgemm_split(mode: int):
+    """SGEMM_SPLIT_PASS (split kernel, then the product kernel) or
+    SGEMM_SPLIT_STREAMED (the product kernel splits its own k-blocks)."""
+    _check(lib().emu_set_sgemm_split(int(mode)))
 
 
 def set_fallback(mode: int):

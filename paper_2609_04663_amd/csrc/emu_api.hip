@@ -47,6 +47,7 @@ hipEvent_t g_switch_event = nullptr;   // orders a new stream after the previous
 int g_split_mode = EMU_SPLIT_SYM;
 int g_split_scope = EMU_SCOPE_OPERAND;
 int g_fallback = EMU_FALLBACK_NONE;
+int g_sgemm_split = EMU_SGEMM_SPLIT_PASS;
 std::string g_err;
 
 // Workspace: [status word (offset 0), the FP64 split state slots of two
@@ -288,6 +289,13 @@ int emu_set_fallback(int mode) {
     return EMU_OK;
 }
 
+int emu_set_sgemm_split(int mode) {
+    if (mode != EMU_SGEMM_SPLIT_PASS && mode != EMU_SGEMM_SPLIT_STREAMED)
+        return fail(EMU_EINVAL, "mode must be EMU_SGEMM_SPLIT_PASS or EMU_SGEMM_SPLIT_STREAMED");
+    g_sgemm_split = mode;
+    return EMU_OK;
+}
+
 int emu_set_split_scope(int scope) {
     if (scope != EMU_SCOPE_OPERAND && scope != EMU_SCOPE_ROWCOL && scope != EMU_SCOPE_KBIN)
         return fail(EMU_EINVAL,
@@ -389,6 +397,21 @@ int emu_sgemm_ex(char transa, char transb, int64_t M, int64_t N, int64_t K, floa
     if (K == 0 || alpha == 0.0f) {
         hipError_t e = launch_scale_c_f32(C, M, N, ldc, beta, g_stream);
         return e == hipSuccess ? EMU_OK : hip_fail(e, "scale C");
+    }
+    if (g_sgemm_split == EMU_SGEMM_SPLIT_STREAMED) {
+        // the product kernel splits the operands itself (128-row tiles)
+        const int splits = sgemm_splits(M, N, (K + KBLK - 1) / KBLK, 128);
+        const size_t part_bytes = splits > 1 ? (size_t)splits * M * N * sizeof(float) : 0;
+        rc = ensure_workspace(part_bytes > 0 ? part_bytes : 1);
+        if (rc) return rc;
+        float *part = splits > 1 ? reinterpret_cast<float *>(ws_planes(0)) : nullptr;
+        prof_mark(0);
+        prof_mark(1);
+        hipError_t e = launch_gemm_f32_streamed(A, lda, ta, B, ldb, tb, C, M, N, K, ldc, alpha,
+                                                beta, splits, part, ws_status(), g_stream);
+        if (e != hipSuccess) return hip_fail(e, "gemm_f32_streamed");
+        prof_mark(2);
+        return EMU_OK;
     }
     const int tile_m = sgemm_tile_m(M, N, (K + KBLK - 1) / KBLK);
     const Shape s = plan(M, N, K, 3, tile_m, SGEMM_NT);

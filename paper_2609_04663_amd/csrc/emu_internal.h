@@ -105,6 +105,66 @@ struct F64SplitOperand {
 
 constexpr int V_ZERO = (int)0x80000000;   // level whose residual is identically zero
 
+typedef unsigned short u16;
+typedef u16 u16x8 __attribute__((ext_vector_type(8)));
+
+// Round a binary32 to BF16, nearest, ties to even, on the bit pattern (a NaN
+// stays a NaN).  Written with selects, not branches: the streamed-split GEMM
+// runs it between its matrix instructions.
+__device__ inline u16 bf16_rne_bits(float x) {
+    const uint32_t u = __float_as_uint(x);
+    const uint32_t rne = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+    const uint32_t nan = (u >> 16) | 0x0040u;
+    return (u16)(((u & 0x7FFFFFFFu) > 0x7F800000u) ? nan : rne);
+}
+
+__device__ inline float bf16_to_float(u16 h) { return __uint_as_float((uint32_t)h << 16); }
+
+// Status of one stored component: overflow, nonzero subnormal, or underflowed
+// to zero from a nonzero source.
+__device__ inline unsigned classify(u16 h, bool src_nonzero) {
+    const unsigned ex = (h >> 7) & 0xFFu, fr = h & 0x7Fu;
+    return (ex == 0xFFu ? ST_OVERFLOW : 0u) |
+           ((ex == 0u && (fr != 0u || src_nonzero)) ? ST_SUBNORMAL : 0u);
+}
+
+// The three BF16 components of an FP32 value (Eq. fp32split, Sec. 4.2):
+// A_r = fl_BF16(A^(r)), A^(r+1) = fl_32(A^(r) - A_r), r = 0, 1, 2, with the
+// input-domain status bits (a non-finite input; a component that overflows,
+// is subnormal or underflows; a nonzero residual after the third).  The split
+// kernel and the streamed-split SGEMM both use it.
+__device__ inline void split3_f32(float a, u16 &c0, u16 &c1, u16 &c2, unsigned &st) {
+    {
+        const bool fin = __builtin_isfinite(a);
+        float r = a;
+        const u16 h0 = bf16_rne_bits(r);
+        unsigned f = classify(h0, r != 0.0f);
+        r = r - bf16_to_float(h0);
+        const u16 h1 = bf16_rne_bits(r);
+        f |= classify(h1, r != 0.0f);
+        r = r - bf16_to_float(h1);
+        const u16 h2 = bf16_rne_bits(r);
+        f |= classify(h2, r != 0.0f);
+        r = r - bf16_to_float(h2);
+        f |= (__builtin_isfinite(r) && r != 0.0f) ? ST_SUBNORMAL : 0u;
+        st |= fin ? f : ST_NAN;
+        c0 = h0;
+        c1 = h1;
+        c2 = h2;
+    }
+}
+__device__ inline void split3_f32x8(const float (&x)[8], u16x8 &c0, u16x8 &c1, u16x8 &c2,
+                                    unsigned &st) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        u16 h0, h1, h2;
+        split3_f32(x[i], h0, h1, h2, st);
+        c0[i] = h0;
+        c1[i] = h1;
+        c2[i] = h2;
+    }
+}
+
 }  // namespace emu
 
 // Launch wrappers (defined in the .hip files, called by the host API).
@@ -163,6 +223,13 @@ hipError_t launch_axpby_f64(const double *P, int64_t ldp, double *C, int64_t ldc
 int device_cu_count();
 int sgemm_tile_m(int64_t M, int64_t N, int64_t KB);   // 192 or 128 output rows per tile
 int sgemm_splits(int64_t M, int64_t N, int64_t KB, int tile_m);
+// The streamed-split SGEMM: op(A) op(B) read in FP32 by the GEMM, split per
+// k-block in the workgroup (128 x 128 tiles); same result bits as the split
+// kernel followed by launch_gemm_f32 with 128-row tiles and the same splits.
+hipError_t launch_gemm_f32_streamed(const float *A, int64_t lda, bool ta, const float *B,
+                                    int64_t ldb, bool tb, float *C, int64_t M, int64_t N,
+                                    int64_t K, int64_t ldc, float alpha, float beta, int splits,
+                                    float *part, unsigned *status, hipStream_t s);
 hipError_t launch_gemm_f32(const uint16_t *Ap, const uint16_t *Bp, float *C, int64_t M, int64_t N,
                            int64_t KB, int64_t RpadA, int64_t RpadB, int64_t ldc, float alpha,
                            float beta, int tile_m, int splits, float *part, hipStream_t s);

@@ -9,29 +9,8 @@
 namespace emu {
 namespace {
 
-typedef unsigned short u16;
-typedef u16 u16x8 __attribute__((ext_vector_type(8)));
-
 constexpr int SPLIT_THREADS = 256;
 constexpr int ROWS_PER_BLOCK = 64;    // 64 packed rows x 4 chunks = 256 work items
-
-// Round a binary32 to BF16, nearest, ties to even, on the bit pattern.
-__device__ inline u16 bf16_rne_bits(float x) {
-    uint32_t u = __float_as_uint(x);
-    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u16)((u >> 16) | 0x0040u);   // NaN stays NaN
-    return (u16)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
-}
-
-__device__ inline float bf16_to_float(u16 h) { return __uint_as_float((uint32_t)h << 16); }
-
-// Status of one stored component: overflow, nonzero subnormal, or underflowed
-// to zero from a nonzero source.
-__device__ inline unsigned classify(u16 h, bool src_nonzero) {
-    unsigned ex = (h >> 7) & 0xFFu, fr = h & 0x7Fu;
-    if (ex == 0xFFu) return ST_OVERFLOW;
-    if (ex == 0u && (fr != 0u || src_nonzero)) return ST_SUBNORMAL;
-    return 0u;
-}
 
 __device__ inline unsigned block_or(unsigned v) {
     // OR within the wave, then one atomic per wave.
@@ -94,24 +73,7 @@ __device__ __forceinline__ void split_f32_operand(const float *__restrict__ X, i
                 x[i] = (ic.prow < prow_lim && k0 + i < k_lim) ? X[(k0 + i) * ldx + ic.prow] : 0.0f;
         }
         u16x8 c0, c1, c2;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const float a = x[i];
-            const bool fin = __builtin_isfinite(a);
-            if (!fin) st |= ST_NAN;
-            float r = a;
-            const u16 h0 = bf16_rne_bits(r);
-            if (fin) st |= classify(h0, r != 0.0f);
-            r = r - bf16_to_float(h0);
-            const u16 h1 = bf16_rne_bits(r);
-            if (fin) st |= classify(h1, r != 0.0f);
-            r = r - bf16_to_float(h1);
-            const u16 h2 = bf16_rne_bits(r);
-            if (fin) st |= classify(h2, r != 0.0f);
-            r = r - bf16_to_float(h2);
-            if (fin && __builtin_isfinite(r) && r != 0.0f) st |= ST_SUBNORMAL;
-            c0[i] = h0; c1[i] = h1; c2[i] = h2;
-        }
+        split3_f32x8(x, c0, c1, c2, st);
         *reinterpret_cast<u16x8 *>(P + packed_index(0, ic.kb, ic.prow, ic.q, KB, Rpad)) = c0;
         *reinterpret_cast<u16x8 *>(P + packed_index(1, ic.kb, ic.prow, ic.q, KB, Rpad)) = c1;
         *reinterpret_cast<u16x8 *>(P + packed_index(2, ic.kb, ic.prow, ic.q, KB, Rpad)) = c2;
