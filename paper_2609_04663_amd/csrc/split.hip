@@ -12,6 +12,9 @@ namespace {
 constexpr int SPLIT_THREADS = 256;
 constexpr int ROWS_PER_BLOCK = 64;    // 64 packed rows x 4 chunks = 256 work items
 
+// Zeros that the loads of entries outside an operand read.
+__device__ double g_zero8_f64[8];
+
 __device__ inline unsigned block_or(unsigned v) {
     // OR within the wave, then one atomic per wave.
     for (int off = 32; off > 0; off >>= 1) v |= __shfl_xor(v, off);
@@ -255,10 +258,14 @@ __device__ __forceinline__ void split_f64_pass(const F64SplitOperand op, int64_t
                 x[i + 1] = t.y;
             }
         } else {
+            // branch-free: an entry outside the operand is read from g_zero8_f64,
+            // so the eight loads are issued together
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 const bool ok = ic.prow < prow_lim && k0 + i < k_lim;
-                x[i] = ok ? (AS_B ? X[(k0 + i) * ldx + ic.prow] : X[ic.prow * ldx + k0 + i]) : 0.0;
+                const double *e = ok ? X + (AS_B ? (k0 + i) * ldx + ic.prow : ic.prow * ldx + k0 + i)
+                                     : g_zero8_f64;
+                x[i] = *e;
             }
         }
         if (op.sc) {
