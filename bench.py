@@ -222,9 +222,9 @@ def main():
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run one plain device-to-device copy of this many MiB: the "
                          "reference kernel that scales rocprofv3 FETCH_SIZE/WRITE_SIZE readings")
-    ap.add_argument("--scope", choices=("operand", "rowcol"), default="operand",
-                    help="FP64 split exponents: the paper's operand-wide chain (default) or the "
-                         "scale-aware row/column weights")
+    ap.add_argument("--scope", choices=("operand", "rowcol", "kbin"), default="operand",
+                    help="FP64 split exponents: the paper's operand-wide chain (default), the "
+                         "scale-aware row/column weights, or those with K-binned classes")
     ap.add_argument("--no-native", action="store_true",
                     help="skip timing the vendor library's native FP32/FP64 GEMM (context)")
     ap.add_argument("--no-depths", action="store_true",
@@ -246,7 +246,8 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
-    scope = emu.SCOPE_ROWCOL if args.scope == "rowcol" else emu.SCOPE_OPERAND
+    scope = {"operand": emu.SCOPE_OPERAND, "rowcol": emu.SCOPE_ROWCOL,
+             "kbin": emu.SCOPE_KBIN}[args.scope]
     emu.set_split_scope(scope)
     if args.copy_calibration_mib > 0:
         nbytes = args.copy_calibration_mib << 20
