@@ -166,3 +166,14 @@ def test_binding_needs_gpu_tensors_after_the_shape_checks():
     B = torch.zeros((3, 6), dtype=torch.float64)
     with pytest.raises(TypeError, match="GPU tensor"):
         emu.dgemm(A, B, 6, C=torch.zeros((5, 6), dtype=torch.float64))
+
+
+def test_mode_switch_arguments(L):
+    import paper_2609_04663_amd as emu
+    for bad in (-1, 2):
+        assert L.emu_set_sgemm_split(bad) == emu.EMU_EINVAL
+        assert L.emu_set_fallback(bad) == emu.EMU_EINVAL
+    for mode in (emu.SGEMM_SPLIT_STREAMED, emu.SGEMM_SPLIT_PASS):
+        assert L.emu_set_sgemm_split(mode) == emu.EMU_OK
+    for mode in (emu.FALLBACK_FP64, emu.FALLBACK_NONE):
+        assert L.emu_set_fallback(mode) == emu.EMU_OK
