@@ -142,9 +142,12 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
     // k-block of the last tile it stays on that k-block (in bounds, unused).
     int c_tile = 0, c_kb = 0;
     const char *c_ak, *c_bk;
+    // tiles in groups of 4 tile-rows per XCD (the tiles of this kernel are up
+    // to four times taller than wide; measured 1-10 % less time than groups
+    // of 8 at 16384 x 16384 x 512 and 8192 x 8192 x 1024)
     auto cursor_bases = [&]() {
         int tm, tn;
-        tile_coords_of<8>((int)blockIdx.x + c_tile * G, ntiles, nt_m, nt_n, tm, tn);
+        tile_coords_of<4>((int)blockIdx.x + c_tile * G, ntiles, nt_m, nt_n, tm, tn);
         c_ak = Ag + (int64_t)c_kb * RpadA * 64 + (int64_t)tm * K::MT * 64;
         c_bk = Bg + (int64_t)c_kb * RpadB * 64 + (int64_t)tn * K::NT * 64;
     };
@@ -259,7 +262,7 @@ __global__ __launch_bounds__(256, 1) void gemm_f64_kernel(
 
     for (int it = 0; it < mine; ++it) {
         int tm, tn;
-        tile_coords_of<8>((int)blockIdx.x + it * G, ntiles, nt_m, nt_n, tm, tn);
+        tile_coords_of<4>((int)blockIdx.x + it * G, ntiles, nt_m, nt_n, tm, tn);
         const int64_t m0 = (int64_t)tm * K::MT, n0 = (int64_t)tn * K::NT;
         double acc64[ACC64_LDS ? 1 : BM][16];
 #pragma unroll
